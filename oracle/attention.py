@@ -113,24 +113,29 @@ def lse_merge(o_a, lse_a, o_b, lse_b):
     return ca * o_a + cb * o_b, lse
 
 
-def attention_bwd(cu, q_gpos, q, kv_gpos, k, v, do, scale=None, dtype=torch.float64):
+def attention_bwd(cu, q_gpos, q, kv_gpos, k, v, do, scale=None, rows=None, dtype=torch.float64):
     """dQ [Tq, Hq, d], dK and dV [Tk, Hkv, d] of the full (single-pass)
     attention of queries at ``q_gpos`` over keys at ``kv_gpos``. The key set
-    must contain every key the queries see, so the softmax is complete."""
+    must contain every key the queries see, so the softmax is complete.
+
+    ``rows`` restricts the backward to some queries: dQ is then computed for
+    those rows only (others are zero) and dK/dV hold only their
+    contributions, which is the exact gradient for every key that no other
+    query sees (e.g. all keys of a document whose queries are all in rows)."""
     Tq, Hq, d = q.shape
     Tk, Hkv, _ = k.shape
     G = Hq // Hkv
     scale = 1.0 / math.sqrt(d) if scale is None or scale <= 0 else float(scale)
-    O, LSE = attention_fwd(cu, q_gpos, q, kv_gpos, k, v, scale, dtype=dtype)
+    O, LSE = attention_fwd(cu, q_gpos, q, kv_gpos, k, v, scale, rows=rows, dtype=dtype)
     q = q.to(dtype)
     k = k.to(dtype)
     v = v.to(dtype)
     do = do.to(dtype)
-    D = (do * O).sum(dim=2).T  # [Hq, Tq]
+    D = (do * torch.nan_to_num(O)).sum(dim=2).T  # [Hq, Tq]
     dq = torch.zeros((Tq, Hq, d), dtype=dtype)
     dk = torch.zeros((Tk, Hkv, d), dtype=dtype)
     dv = torch.zeros((Tk, Hkv, d), dtype=dtype)
-    for r, ks, mask in _blocks(cu, q_gpos, kv_gpos, None):
+    for r, ks, mask in _blocks(cu, q_gpos, kv_gpos, rows):
         if ks.size == 0:
             continue
         kt = torch.from_numpy(ks)

@@ -1,0 +1,281 @@
+// C ABI entry points that launch device work. Everything is validated on the
+// host before the first launch; launches are asynchronous on the caller's
+// stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "../kernels/launch.hpp"
+#include "internal.hpp"
+#include "view.hpp"
+
+using fc::fail;
+using fc::View;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int check_view(fc_view view, View*& v) {
+  if (!view) return fail(FC_ERR_INVALID_ARG, "view is null");
+  v = reinterpret_cast<View*>(view);
+  if (!v->dev_meta) return fail(FC_ERR_WORKSPACE, "view is not bound to device metadata");
+  return FC_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return FC_OK;
+  return fail(FC_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+float resolve_scale(float scale, int d) { return scale > 0.f ? scale : 1.f / std::sqrt(float(d)); }
+
+struct FwdWs {
+  size_t o_bytes, l_bytes, total;
+};
+FwdWs fwd_ws(const View& v, int32_t mode) {
+  FwdWs w{};
+  if (mode == FC_TWO_PASS && v.t_recv() > 0) {
+    w.o_bytes = align_up(size_t(v.t_q()) * v.hq * v.d * sizeof(float));
+    w.l_bytes = align_up(size_t(v.t_q()) * v.hq * sizeof(float));
+    w.total = 2 * (w.o_bytes + w.l_bytes);
+  }
+  return w;
+}
+size_t bwd_ws(const View& v) { return align_up(size_t(v.t_q()) * v.hq * sizeof(float)); }
+
+fck::FwdParams fwd_params(const View& v, const int32_t* items, const int32_t* perm, int64_t n,
+                          const void* q, const void* k_loc, const void* v_loc, const void* k_recv,
+                          const void* v_recv, float scale) {
+  fck::FwdParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k_loc = static_cast<const uint16_t*>(k_loc);
+  p.v_loc = static_cast<const uint16_t*>(v_loc);
+  p.k_recv = static_cast<const uint16_t*>(k_recv);
+  p.v_recv = static_cast<const uint16_t*>(v_recv);
+  p.items = items;
+  p.perm = perm;
+  p.n_items = int32_t(n);
+  p.hq = v.hq;
+  p.hkv = v.hkv;
+  p.group = v.hq / v.hkv;
+  p.head_chunks = p.group / v.heads_per_tile;
+  p.scale_log2 = resolve_scale(scale, v.d) * 1.4426950408889634f;
+  p.t_q = v.t_q();
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fc_workspace_size(fc_view view, int32_t mode, size_t* fwd_bytes, size_t* bwd_bytes) {
+  fc::clear_error();
+  if (!view) return fail(FC_ERR_INVALID_ARG, "view is null");
+  if (mode != FC_TWO_PASS && mode != FC_FUSED) return fail(FC_ERR_INVALID_ARG, "bad mode");
+  const View& v = *reinterpret_cast<View*>(view);
+  if (fwd_bytes) *fwd_bytes = fwd_ws(v, mode).total;
+  if (bwd_bytes) *bwd_bytes = bwd_ws(v);
+  return FC_OK;
+}
+
+int fc_kv_gather(fc_view view, const void* k_packed, const void* v_packed, int64_t t_packed,
+                 void* k_loc, void* v_loc, void* k_recv, void* v_recv, void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (v->t_q() + v->t_recv() == 0) return FC_OK;
+  if (!k_packed || !v_packed || (v->t_q() && (!k_loc || !v_loc)) ||
+      (v->t_recv() && (!k_recv || !v_recv)))
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  // every gathered position must lie inside the packed tensors
+  int64_t max_pos = -1;
+  if (v->t_q()) max_pos = std::max<int64_t>(max_pos, v->q_gpos.back());
+  if (v->t_recv()) max_pos = std::max<int64_t>(max_pos, v->recv_gpos.back());
+  if (max_pos >= t_packed)
+    return fail(FC_ERR_SHAPE, "packed K/V have " + std::to_string(t_packed) +
+                                  " rows, the view reads row " + std::to_string(max_pos));
+  const int32_t* m = v->dev_meta;
+  return hip_status(
+      fck::launch_kv_gather(static_cast<const uint16_t*>(k_packed),
+                            static_cast<const uint16_t*>(v_packed), m + v->off.q_gpos,
+                            m + v->off.recv_gpos, v->t_q(), v->t_recv(), v->hkv * v->d,
+                            static_cast<uint16_t*>(k_loc), static_cast<uint16_t*>(v_loc),
+                            static_cast<uint16_t*>(k_recv), static_cast<uint16_t*>(v_recv),
+                            reinterpret_cast<hipStream_t>(stream)),
+      "kv_gather launch");
+}
+
+int fc_attn_fwd_partial(fc_view view, int32_t src, const void* q, const void* k_src,
+                        const void* v_src, float scale, float* o_part, float* lse_part,
+                        void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (src != 0 && src != 1) return fail(FC_ERR_INVALID_ARG, "src must be 0 or 1");
+  if (v->t_q() == 0) return FC_OK;
+  const bool have_keys = src == 0 ? true : v->t_recv() > 0;
+  if (!q || !o_part || !lse_part || (have_keys && (!k_src || !v_src)))
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  const int32_t* m = v->dev_meta;
+  fck::FwdParams p =
+      src == 0 ? fwd_params(*v, m + v->off.fwd_local, m + v->off.perm_fwd_local,
+                            int64_t(v->fwd_local.size() / 8), q, k_src, v_src, nullptr, nullptr,
+                            scale)
+               : fwd_params(*v, m + v->off.fwd_recv, m + v->off.perm_fwd_recv,
+                            int64_t(v->fwd_recv.size() / 8), q, nullptr, nullptr, k_src, v_src,
+                            scale);
+  p.o_f32 = o_part;
+  p.lse = lse_part;
+  return hip_status(fck::launch_fwd(p, v->d, v->heads_per_tile, false,
+                                    reinterpret_cast<hipStream_t>(stream)),
+                    "attn_fwd launch");
+}
+
+int fc_attn_fwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                const void* k_recv, const void* v_recv, float scale, int32_t mode, void* o,
+                float* o_f32, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (mode != FC_TWO_PASS && mode != FC_FUSED) return fail(FC_ERR_INVALID_ARG, "bad mode");
+  if (v->t_q() == 0) return FC_OK;
+  if (!q || !k_loc || !v_loc || !o || !lse || (v->t_recv() && (!k_recv || !v_recv)))
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  const FwdWs w = fwd_ws(*v, mode);
+  if (ws_bytes < w.total || (w.total && !ws))
+    return fail(FC_ERR_WORKSPACE, "forward workspace of " + std::to_string(ws_bytes) +
+                                      " bytes, need " + std::to_string(w.total));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int32_t* m = v->dev_meta;
+  if (mode == FC_FUSED || v->t_recv() == 0) {
+    // one pass: both sources (fused items), or the local source alone
+    const bool fused = mode == FC_FUSED && v->t_recv() > 0;
+    fck::FwdParams p =
+        fused ? fwd_params(*v, m + v->off.fwd_fused, m + v->off.perm_fwd_fused,
+                           int64_t(v->fwd_fused.size() / 8), q, k_loc, v_loc, k_recv, v_recv, scale)
+              : fwd_params(*v, m + v->off.fwd_local, m + v->off.perm_fwd_local,
+                           int64_t(v->fwd_local.size() / 8), q, k_loc, v_loc, nullptr, nullptr,
+                           scale);
+    p.o_bf16 = static_cast<uint16_t*>(o);
+    p.o_f32 = o_f32;
+    p.lse = lse;
+    return hip_status(fck::launch_fwd(p, v->d, v->heads_per_tile, true, s), "attn_fwd launch");
+  }
+  char* base = static_cast<char*>(ws);
+  float* oa = reinterpret_cast<float*>(base);
+  float* ob = reinterpret_cast<float*>(base + w.o_bytes);
+  float* la = reinterpret_cast<float*>(base + 2 * w.o_bytes);
+  float* lb = reinterpret_cast<float*>(base + 2 * w.o_bytes + w.l_bytes);
+  fck::FwdParams pl = fwd_params(*v, m + v->off.fwd_local, m + v->off.perm_fwd_local,
+                                 int64_t(v->fwd_local.size() / 8), q, k_loc, v_loc, nullptr,
+                                 nullptr, scale);
+  pl.o_f32 = oa;
+  pl.lse = la;
+  if (int rc = hip_status(fck::launch_fwd(pl, v->d, v->heads_per_tile, false, s), "local pass"))
+    return rc;
+  fck::FwdParams pr = fwd_params(*v, m + v->off.fwd_recv, m + v->off.perm_fwd_recv,
+                                 int64_t(v->fwd_recv.size() / 8), q, nullptr, nullptr, k_recv,
+                                 v_recv, scale);
+  pr.o_f32 = ob;
+  pr.lse = lb;
+  if (int rc = hip_status(fck::launch_fwd(pr, v->d, v->heads_per_tile, false, s), "recv pass"))
+    return rc;
+  return hip_status(fck::launch_lse_merge(oa, la, ob, lb, v->t_q(), v->hq, v->d,
+                                          static_cast<uint16_t*>(o), o_f32, lse, s),
+                    "lse_merge launch");
+}
+
+int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const float* lse_b,
+                 int32_t t, int32_t h, int32_t d, void* o_bf16, float* o_f32, float* lse_out,
+                 void* stream) {
+  fc::clear_error();
+  if (t < 0 || h < 0) return fail(FC_ERR_INVALID_ARG, "negative size");
+  if (d != 64 && d != 128) return fail(FC_ERR_UNSUPPORTED, "head dim must be 64 or 128");
+  if (int64_t(t) * h == 0) return FC_OK;
+  if (!o_a || !lse_a || !o_b || !lse_b || !o_bf16 || !lse_out)
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  return hip_status(fck::launch_lse_merge(o_a, lse_a, o_b, lse_b, t, h, d,
+                                          static_cast<uint16_t*>(o_bf16), o_f32, lse_out,
+                                          reinterpret_cast<hipStream_t>(stream)),
+                    "lse_merge launch");
+}
+
+int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta, float* dq,
+                      void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (v->t_q() == 0) return FC_OK;
+  if (!o || !dout || !delta || !dq) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  return hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o),
+                                               static_cast<const uint16_t*>(dout), delta, dq,
+                                               v->t_q(), v->hq, v->d,
+                                               reinterpret_cast<hipStream_t>(stream)),
+                    "bwd preprocess launch");
+}
+
+int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                     const void* k_recv, const void* v_recv, const float* lse, const float* delta,
+                     const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
+                     float* dk_recv, float* dv_recv, void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (v->t_q() == 0) return FC_OK;
+  if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dq || !dk_loc || !dv_loc ||
+      (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  const int32_t* m = v->dev_meta;
+  fck::BwdParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.dout = static_cast<const uint16_t*>(dout);
+  p.lse = lse;
+  p.delta = delta;
+  p.k_loc = static_cast<const uint16_t*>(k_loc);
+  p.v_loc = static_cast<const uint16_t*>(v_loc);
+  p.k_recv = static_cast<const uint16_t*>(k_recv);
+  p.v_recv = static_cast<const uint16_t*>(v_recv);
+  p.items = m + v->off.bwd;
+  p.perm = m + v->off.perm_bwd;
+  p.lim = m + v->off.lim;
+  p.n_items = int32_t(v->bwd.size() / 8);
+  p.hq = v->hq;
+  p.hkv = v->hkv;
+  p.group = v->hq / v->hkv;
+  p.scale = resolve_scale(scale, v->d);
+  p.dq = dq;
+  p.dk_loc = dk_loc;
+  p.dv_loc = dv_loc;
+  p.dk_recv = dk_recv;
+  p.dv_recv = dv_recv;
+  p.t_q = v->t_q();
+  return hip_status(fck::launch_bwd(p, v->d, reinterpret_cast<hipStream_t>(stream)),
+                    "attn_bwd launch");
+}
+
+int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                const void* k_recv, const void* v_recv, const void* o, const float* lse,
+                const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
+                float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes, void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (v->t_q() == 0) return FC_OK;
+  const size_t need = bwd_ws(*v);
+  if (!ws || ws_bytes < need)
+    return fail(FC_ERR_WORKSPACE, "backward workspace of " + std::to_string(ws_bytes) +
+                                      " bytes, need " + std::to_string(need));
+  if (!o) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  float* delta = static_cast<float*>(ws);
+  // validate the pass's arguments before the first launch
+  if (!q || !k_loc || !v_loc || !lse || !dout || !dq || !dk_loc || !dv_loc ||
+      (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  if (int rc = fc_bwd_preprocess(view, o, dout, delta, dq, stream)) return rc;
+  return fc_attn_bwd_pass(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq,
+                          dk_loc, dv_loc, dk_recv, dv_recv, stream);
+}
+
+}  // extern "C"

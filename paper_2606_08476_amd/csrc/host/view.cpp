@@ -1,0 +1,299 @@
+// Rank view and tile maps (host side).
+//
+// A rank's queries are its shards' tokens in ascending global position
+// ("local order"). Under the document mask (Sec. 2.1) a query sees the
+// earlier tokens of its own document, so the KV a rank must hold is, per
+// document, the prefix up to its last held token; the part it does not hold
+// is its sharding-aware receive set (Sec. 3.2), stored compacted in
+// ascending position.
+//
+// Two consequences shape the kernels' work lists:
+//   * the rank's tokens of one document ("segment") are contiguous in local
+//     order, and a query at local index i sees exactly the local keys
+//     seg_start..i: the local pass is ordinary variable-length causal
+//     attention over the segments;
+//   * inside a maximal run of held positions ("piece") no received token
+//     occurs, so every query of the piece sees the same first n_P received
+//     tokens of its document: the received pass is mask-free per piece.
+// Tiles that no query of a block can see are never listed.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <numeric>
+
+#include "internal.hpp"
+#include "view.hpp"
+
+namespace fc {
+
+namespace {
+
+int32_t ceil_div(int64_t a, int64_t b) { return int32_t((a + b - 1) / b); }
+
+// First tile start q0 + t*bm at or after `from`, or q1 if there is none.
+int32_t first_tile_at_or_after(int32_t q0, int32_t q1, int32_t bm, int64_t from) {
+  if (from <= q0) return q0;
+  const int64_t t = q0 + int64_t(bm) * ceil_div(from - q0, bm);
+  return t >= q1 ? q1 : int32_t(t);
+}
+
+std::vector<int32_t> lpt_order(const std::vector<int64_t>& cost) {
+  std::vector<int32_t> idx(cost.size());
+  std::iota(idx.begin(), idx.end(), 0);
+  std::stable_sort(idx.begin(), idx.end(),
+                   [&](int32_t a, int32_t b) { return cost[a] > cost[b]; });
+  return idx;
+}
+
+}  // namespace
+
+void View::build_tiles() {
+  const int32_t S = int32_t(seg_doc.size());
+  auto ldiag_of = [&](int32_t s0, int32_t t0) {
+    // key tiles s0 + j*bn with s0 + j*bn + bn - 1 <= t0 are seen whole by
+    // every row of a query tile starting at t0
+    return s0 + ((t0 - s0 + 1) / bn_fwd) * bn_fwd;
+  };
+  auto push8 = [](std::vector<int32_t>& v, std::initializer_list<int32_t> x) {
+    v.insert(v.end(), x.begin(), x.end());
+  };
+  // forward, local pass: query tiles per segment
+  for (int32_t s = 0; s < S; ++s) {
+    const int32_t s0 = q_cu[s], s1 = q_cu[s + 1];
+    for (int32_t t0 = s0; t0 < s1; t0 += bm_fwd) {
+      const int32_t t1 = std::min(t0 + bm_fwd, s1);
+      push8(fwd_local, {t0, t1, 0, 0, s0, t1, ldiag_of(s0, t0), s});
+    }
+  }
+  // forward, received and fused passes: query tiles per piece
+  for (size_t p = 0; p < pieces.size() / 5; ++p) {
+    const int32_t s = pieces[5 * p], qs = pieces[5 * p + 1], qe = pieces[5 * p + 2];
+    const int32_t np = pieces[5 * p + 4];
+    const int32_t r0 = recv_cu[s], s0 = q_cu[s];
+    for (int32_t t0 = qs; t0 < qe; t0 += bm_fwd) {
+      const int32_t t1 = std::min(t0 + bm_fwd, qe);
+      push8(fwd_recv, {t0, t1, r0, r0 + np, 0, 0, 0, s});
+      push8(fwd_fused, {t0, t1, r0, r0 + np, s0, t1, ldiag_of(s0, t0), s});
+    }
+  }
+  // backward, key-major: local key tiles then received key tiles
+  for (int32_t s = 0; s < S; ++s) {
+    const int32_t s0 = q_cu[s], s1 = q_cu[s + 1];
+    for (int32_t k0 = s0; k0 < s1; k0 += bn_bwd) {
+      const int32_t k1 = std::min(k0 + bn_bwd, s1);
+      // rows i >= k0 see key k0; rows i >= k1-1 see the whole tile
+      push8(bwd, {k0, k1, k0, s1, first_tile_at_or_after(k0, s1, bm_bwd, k1 - 1), 0, s, 0});
+    }
+  }
+  for (int32_t s = 0; s < S; ++s) {
+    const int32_t s1 = q_cu[s + 1];
+    const int32_t rl = recv_cu[s], rh = recv_cu[s + 1];
+    // the segment's pieces in local order have non-decreasing n_P
+    const int32_t pa = seg_piece[s], pb = seg_piece[s + 1];
+    for (int32_t k0 = rl; k0 < rh; k0 += bn_bwd) {
+      const int32_t k1 = std::min(k0 + bn_bwd, rh);
+      int32_t q0 = s1, qa = s1;
+      for (int32_t p = pa; p < pb; ++p) {
+        const int32_t lim_p = rl + pieces[5 * p + 4];
+        if (q0 == s1 && lim_p > k0) q0 = pieces[5 * p + 1];
+        if (lim_p >= k1) {
+          qa = pieces[5 * p + 1];
+          break;
+        }
+      }
+      push8(bwd, {k0, k1, q0, s1, first_tile_at_or_after(q0, s1, bm_bwd, qa), 1, s, 0});
+    }
+  }
+  // largest-first launch orders (the lists themselves stay in map order)
+  auto fwd_cost = [&](const std::vector<int32_t>& items) {
+    std::vector<int64_t> c(items.size() / 8);
+    for (size_t i = 0; i < c.size(); ++i) {
+      const int32_t* it = &items[8 * i];
+      c[i] = ceil_div(it[3] - it[2], bn_fwd) + ceil_div(it[5] - it[4], bn_fwd);
+    }
+    return c;
+  };
+  perm_fwd_local = lpt_order(fwd_cost(fwd_local));
+  perm_fwd_recv = lpt_order(fwd_cost(fwd_recv));
+  perm_fwd_fused = lpt_order(fwd_cost(fwd_fused));
+  std::vector<int64_t> bc(bwd.size() / 8);
+  for (size_t i = 0; i < bc.size(); ++i) bc[i] = ceil_div(bwd[8 * i + 3] - bwd[8 * i + 2], bm_bwd);
+  perm_bwd = lpt_order(bc);
+}
+
+void View::build_meta() {
+  meta.clear();
+  auto put = [&](const std::vector<int32_t>& v) {
+    const int64_t off = int64_t(meta.size());
+    meta.insert(meta.end(), v.begin(), v.end());
+    meta.resize((meta.size() + 63) / 64 * 64, 0);  // 256-byte aligned sections
+    return off;
+  };
+  off.fwd_local = put(fwd_local);
+  off.fwd_recv = put(fwd_recv);
+  off.fwd_fused = put(fwd_fused);
+  off.bwd = put(bwd);
+  off.perm_fwd_local = put(perm_fwd_local);
+  off.perm_fwd_recv = put(perm_fwd_recv);
+  off.perm_fwd_fused = put(perm_fwd_fused);
+  off.perm_bwd = put(perm_bwd);
+  off.q_gpos = put(q_gpos);
+  off.recv_gpos = put(recv_gpos);
+  off.lim = put(lim);
+  if (meta.empty()) meta.resize(64, 0);
+}
+
+int build_view(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_t n_shards,
+               int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d, View& v) {
+  std::vector<int64_t> lens;
+  if (int rc = doc_lengths(cu, n_docs, lens)) return rc;
+  if (int rc = validate_plan(lens, cp, shards, n_shards, false)) return rc;
+  if (rank < 0 || rank >= cp) return fail(FC_ERR_INVALID_ARG, "rank out of range");
+  if (d != 64 && d != 128) return fail(FC_ERR_UNSUPPORTED, "head dim must be 64 or 128");
+  if (hq < 1 || hkv < 1 || hq % hkv)
+    return fail(FC_ERR_INVALID_ARG, "need hq, hkv >= 1 and hq % hkv == 0");
+  const int32_t G = hq / hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(FC_ERR_UNSUPPORTED, "hq/hkv must be 1, 2, 4 or 8");
+  if (int64_t(cu[n_docs]) > (int64_t(1) << 30))
+    return fail(FC_ERR_UNSUPPORTED, "context longer than 2^30 tokens");
+  v.hq = hq;
+  v.hkv = hkv;
+  v.d = d;
+  v.heads_per_tile = std::min(G, 4);
+  v.bm_fwd = 32 * (4 / v.heads_per_tile);
+  v.bn_fwd = 64;
+  v.bm_bwd = 32;
+  v.bn_bwd = 128;
+
+  std::vector<fc_shard> mine;
+  for (int64_t i = 0; i < n_shards; ++i)
+    if (shards[i].rank == rank) mine.push_back(shards[i]);
+  std::sort(mine.begin(), mine.end(), [](const fc_shard& a, const fc_shard& b) {
+    return a.doc != b.doc ? a.doc < b.doc : a.offset < b.offset;
+  });
+  v.q_cu.assign(1, 0);
+  v.recv_cu.assign(1, 0);
+  v.seg_piece.assign(1, 0);
+  for (size_t i = 0; i < mine.size();) {
+    const int32_t doc = mine[i].doc, c0 = cu[doc];
+    const int32_t seg = int32_t(v.seg_doc.size());
+    v.seg_doc.push_back(doc);
+    int32_t held_end = 0;  // offset just past the previous piece
+    int32_t gap_total = 0; // received tokens of this document so far
+    while (i < mine.size() && mine[i].doc == doc) {
+      // one piece: a maximal run of consecutive held offsets
+      const int32_t a = mine[i].offset;
+      int32_t b = a + mine[i].len;
+      ++i;
+      while (i < mine.size() && mine[i].doc == doc && mine[i].offset == b) b += mine[i++].len;
+      for (int32_t u = held_end; u < a; ++u) v.recv_gpos.push_back(c0 + u);
+      gap_total += a - held_end;
+      const int32_t qs = int32_t(v.q_gpos.size());
+      for (int32_t u = a; u < b; ++u) v.q_gpos.push_back(c0 + u);
+      const int32_t qe = int32_t(v.q_gpos.size());
+      v.pieces.insert(v.pieces.end(), {seg, qs, qe, c0 + a, gap_total});
+      v.lim.insert(v.lim.end(), size_t(qe - qs), v.recv_cu[seg] + gap_total);
+      v.pairs_recv += int64_t(qe - qs) * gap_total;
+      held_end = b;
+    }
+    v.q_cu.push_back(int32_t(v.q_gpos.size()));
+    v.recv_cu.push_back(int32_t(v.recv_gpos.size()));
+    v.seg_piece.push_back(int32_t(v.pieces.size() / 5));
+    const int64_t seg_len = v.q_cu[seg + 1] - v.q_cu[seg];
+    v.pairs_loc += seg_len * (seg_len + 1) / 2;
+  }
+  v.build_tiles();
+  v.build_meta();
+  return FC_OK;
+}
+
+}  // namespace fc
+
+using namespace fc;
+
+extern "C" {
+
+int fc_view_create(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_t n_shards,
+                   int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d, fc_view* out) {
+  clear_error();
+  if (!out) return fail(FC_ERR_INVALID_ARG, "out is null");
+  *out = nullptr;
+  View* v = new View();
+  if (int rc = build_view(cu, n_docs, shards, n_shards, cp, rank, hq, hkv, d, *v)) {
+    delete v;
+    return rc;
+  }
+  *out = reinterpret_cast<fc_view>(v);
+  return FC_OK;
+}
+
+int fc_view_get_info(fc_view view, fc_view_info* out) {
+  clear_error();
+  if (!view || !out) return fail(FC_ERR_INVALID_ARG, "null argument");
+  const View& v = *reinterpret_cast<View*>(view);
+  *out = fc_view_info{};
+  out->t_q = int32_t(v.q_gpos.size());
+  out->t_recv = int32_t(v.recv_gpos.size());
+  out->n_seg = int32_t(v.seg_doc.size());
+  out->n_pieces = int32_t(v.pieces.size() / 5);
+  out->hq = v.hq;
+  out->hkv = v.hkv;
+  out->d = v.d;
+  out->bm_fwd = v.bm_fwd;
+  out->bn_fwd = v.bn_fwd;
+  out->bm_bwd = v.bm_bwd;
+  out->bn_bwd = v.bn_bwd;
+  out->n_fwd_local = int64_t(v.fwd_local.size() / 8);
+  out->n_fwd_recv = int64_t(v.fwd_recv.size() / 8);
+  out->n_fwd_fused = int64_t(v.fwd_fused.size() / 8);
+  out->n_bwd = int64_t(v.bwd.size() / 8);
+  out->pairs_loc = v.pairs_loc;
+  out->pairs_recv = v.pairs_recv;
+  out->meta_bytes = int64_t(v.meta.size() * sizeof(int32_t));
+  return FC_OK;
+}
+
+int fc_view_export(fc_view view, int32_t* q_gpos, int32_t* recv_gpos, int32_t* seg_doc,
+                   int32_t* q_cu_docseg, int32_t* recv_cu, int32_t* pieces, int32_t* lim,
+                   int32_t* fwd_local, int32_t* fwd_recv, int32_t* fwd_fused, int32_t* bwd) {
+  clear_error();
+  if (!view) return fail(FC_ERR_INVALID_ARG, "view is null");
+  const View& v = *reinterpret_cast<View*>(view);
+  auto cp = [](int32_t* dst, const std::vector<int32_t>& src) {
+    if (dst) std::copy(src.begin(), src.end(), dst);
+  };
+  cp(q_gpos, v.q_gpos);
+  cp(recv_gpos, v.recv_gpos);
+  cp(seg_doc, v.seg_doc);
+  cp(q_cu_docseg, v.q_cu);
+  cp(recv_cu, v.recv_cu);
+  cp(pieces, v.pieces);
+  cp(lim, v.lim);
+  cp(fwd_local, v.fwd_local);
+  cp(fwd_recv, v.fwd_recv);
+  cp(fwd_fused, v.fwd_fused);
+  cp(bwd, v.bwd);
+  return FC_OK;
+}
+
+int fc_view_bind(fc_view view, void* dev_meta, size_t bytes, void* stream) {
+  clear_error();
+  if (!view || !dev_meta) return fail(FC_ERR_INVALID_ARG, "null argument");
+  View& v = *reinterpret_cast<View*>(view);
+  const size_t need = v.meta.size() * sizeof(int32_t);
+  if (bytes < need)
+    return fail(FC_ERR_WORKSPACE, "metadata buffer of " + std::to_string(bytes) +
+                                      " bytes, need " + std::to_string(need));
+  if (reinterpret_cast<uintptr_t>(dev_meta) % 256)
+    return fail(FC_ERR_INVALID_ARG, "metadata buffer must be 256-byte aligned");
+  hipError_t e = hipMemcpyAsync(dev_meta, v.meta.data(), need, hipMemcpyHostToDevice,
+                                reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FC_ERR_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+  v.dev_meta = reinterpret_cast<const int32_t*>(dev_meta);
+  return FC_OK;
+}
+
+void fc_view_destroy(fc_view view) { delete reinterpret_cast<View*>(view); }
+
+}  // extern "C"

@@ -1,0 +1,44 @@
+// Host representation of a rank view (the opaque fc_view).
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "flashcp.h"
+
+namespace fc {
+
+struct View {
+  int32_t hq = 0, hkv = 0, d = 0, heads_per_tile = 1;
+  int32_t bm_fwd = 0, bn_fwd = 0, bm_bwd = 0, bn_bwd = 0;
+
+  std::vector<int32_t> q_gpos, recv_gpos;   // global positions, local / receive order
+  std::vector<int32_t> seg_doc, q_cu, recv_cu, seg_piece;
+  std::vector<int32_t> pieces;              // 5 per piece: seg, q_start, q_end, g_start, n_P
+  std::vector<int32_t> lim;                 // receive index end seen by each query
+  int64_t pairs_loc = 0, pairs_recv = 0;
+
+  // work lists, 8 int32 per item (layout documented in flashcp.h)
+  std::vector<int32_t> fwd_local, fwd_recv, fwd_fused, bwd;
+  std::vector<int32_t> perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
+
+  // device blob: every table above that a kernel reads, int32, sections
+  // aligned to 256 bytes; `off` holds section offsets in int32 elements
+  std::vector<int32_t> meta;
+  struct {
+    int64_t fwd_local, fwd_recv, fwd_fused, bwd;
+    int64_t perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
+    int64_t q_gpos, recv_gpos, lim;
+  } off{};
+  const int32_t* dev_meta = nullptr;        // set by fc_view_bind
+
+  int32_t t_q() const { return int32_t(q_gpos.size()); }
+  int32_t t_recv() const { return int32_t(recv_gpos.size()); }
+  void build_tiles();
+  void build_meta();
+};
+
+int build_view(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_t n_shards,
+               int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d, View& v);
+
+}  // namespace fc

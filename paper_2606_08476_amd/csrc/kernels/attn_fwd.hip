@@ -1,0 +1,196 @@
+// Forward attention over one rank's share (gfx950).
+//
+// One workgroup (4 waves) takes one work item -- a tile of query tokens
+// with a received key range (no mask inside it, FlashCP Sec. 3.2: every
+// query of a piece sees the same received prefix) and a local key range
+// (intra-document causal, Sec. 2.1) -- for `heads_per_tile` query heads of
+// one KV head. Each wave owns 32 query rows of one head. Per key tile of 64
+// keys, staged in LDS and shared by the waves (and so by the heads of the
+// group):
+//   S^T = K Q^T        MFMA 32x32x16, Q held in registers (B operand), so a
+//                      query is a lane and its row statistics are per lane;
+//   online softmax     base-2, running max/sum per lane, one cross-half
+//                      exchange per tile;
+//   O^T += V^T P^T     V^T read from LDS with transpose reads, P^T straight
+//                      from the S^T accumulator registers.
+// Output: the final O (bf16, optionally fp32) and LSE, or an fp32 partial
+// O/LSE for the log-sum-exp merge.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace fck {
+
+template <int D, int HPW, bool FINAL>
+__global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams p) {
+  constexpr int BN = 64;        // keys per tile
+  constexpr int WPH = 4 / HPW;  // waves per query head
+  constexpr int KS = D / 16;    // MFMA k-steps over the head dim
+  constexpr int DB = D / 32;    // 32-wide output blocks of the head dim
+  constexpr int LD = D + 8;     // padded LDS row (elements)
+  constexpr int CH = D / 8;     // 16-byte chunks per row
+  __shared__ __attribute__((aligned(16))) u16 sK[BN * LD];
+  __shared__ __attribute__((aligned(16))) u16 sV[BN * LD];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int b = blockIdx.x;
+  const int kvh = b % p.hkv;
+  const int rest = b / p.hkv;
+  const int hc = rest % p.head_chunks;
+  const int32_t* it = p.items + 8 * p.perm[rest / p.head_chunks];
+  const int q0 = it[0], q1 = it[1], r0 = it[2], r1 = it[3], l0 = it[4], l1 = it[5];
+  const int ldiag = it[6];
+
+  const int h = kvh * p.group + hc * HPW + wave / WPH;
+  const int qrow = q0 + (wave % WPH) * 32 + (lane & 31);
+  const bool qvalid = qrow < q1;
+
+  bf16x8 qreg[KS];
+  {
+    const u16* qp = p.q + ((size_t)qrow * p.hq + h) * D + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qreg[ks] = qvalid ? *reinterpret_cast<const bf16x8*>(qp + 16 * ks) : zero8();
+  }
+
+  f32x16 oacc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) oacc[db] = zero16();
+  float m = -INFINITY;  // running row max (log2 units)
+  float lsum = 0.f;     // this lane's share of the row sum
+
+  for (int src = 0; src < 2; ++src) {
+    const int lo = src == 0 ? r0 : l0;
+    const int hi = src == 0 ? r1 : l1;
+    const u16* Kg = src == 0 ? p.k_recv : p.k_loc;
+    const u16* Vg = src == 0 ? p.v_recv : p.v_loc;
+    for (int k0 = lo; k0 < hi; k0 += BN) {
+      __syncthreads();  // the previous tile is consumed
+      for (int c = threadIdx.x; c < BN * CH; c += 256) {
+        const int r = c / CH, cc = c % CH;
+        bf16x8 kv = zero8(), vv = zero8();
+        if (k0 + r < hi) {
+          const size_t g = ((size_t)(k0 + r) * p.hkv + kvh) * D + cc * 8;
+          kv = *reinterpret_cast<const bf16x8*>(Kg + g);
+          vv = *reinterpret_cast<const bf16x8*>(Vg + g);
+        }
+        *reinterpret_cast<bf16x8*>(sK + r * LD + cc * 8) = kv;
+        *reinterpret_cast<bf16x8*>(sV + r * LD + cc * 8) = vv;
+      }
+      __syncthreads();
+
+      f32x16 s[2];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        s[mb] = zero16();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          s[mb] = mfma32(lds_read8(sK, (mb * 32 + (lane & 31)) * LD + 16 * ks + 8 * half),
+                         qreg[ks], s[mb]);
+      }
+      // scale; mask keys past the range and, on diagonal tiles, later keys
+      const bool diag = src == 1 && k0 >= ldiag;
+      const bool edge = diag || k0 + BN > hi;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float x = s[mb][i] * p.scale_log2;
+          if (edge) {
+            const int kr = k0 + mb * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
+            const bool vis = kr < hi && (!diag || kr <= qrow);
+            x = vis ? x : -INFINITY;
+          }
+          s[mb][i] = x;
+          mx = fmaxf(mx, x);
+        }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m, mx);
+      const float mref = mnew == -INFINITY ? 0.f : mnew;
+      const float alpha = exp2f(m - mref);
+      m = mnew;
+      float ps = 0.f;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float e = exp2f(s[mb][i] - mref);
+          s[mb][i] = e;
+          ps += e;
+        }
+      }
+      lsum = lsum * alpha + ps;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+
+      // O^T += V^T P^T, 16 keys per MFMA step
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const bf16x8 pb = pack8(s[kk >> 1], 8 * (kk & 1));
+        const int rb = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * half;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          oacc[db] = mfma32(lds_operand_tr(sV, LD, rb, rb + 8, 32 * db, lane), pb, oacc[db]);
+      }
+    }
+  }
+
+  lsum += __shfl_xor(lsum, 32);
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  const float lse = lsum > 0.f ? (m + log2f(lsum)) * kLn2 : -INFINITY;
+  if (qvalid) {
+    const size_t ob = ((size_t)qrow * p.hq + h) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int dcol = 32 * db + 8 * g + 4 * half;
+        f32x4 v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = oacc[db][4 * g + j] * inv;
+        if (FINAL) {
+          uint2 packed;
+          packed.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
+          packed.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
+          *reinterpret_cast<uint2*>(p.o_bf16 + ob + dcol) = packed;
+        }
+        if (!FINAL || p.o_f32) *reinterpret_cast<f32x4*>(p.o_f32 + ob + dcol) = v;
+      }
+    }
+    if (half == 0) p.lse[(size_t)h * p.t_q + qrow] = lse;
+  }
+}
+
+template <int D, int HPW>
+static hipError_t launch_fwd_t(const FwdParams& p, bool final_out, hipStream_t s) {
+  const dim3 grid(unsigned(p.n_items) * p.hkv * p.head_chunks), block(256);
+  if (final_out)
+    hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, true>), grid, block, 0, s, p);
+  else
+    hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, false>), grid, block, 0, s, p);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_fwd_d(const FwdParams& p, int hpw, bool final_out, hipStream_t s) {
+  switch (hpw) {
+    case 1: return launch_fwd_t<D, 1>(p, final_out, s);
+    case 2: return launch_fwd_t<D, 2>(p, final_out, s);
+    case 4: return launch_fwd_t<D, 4>(p, final_out, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_fwd(const FwdParams& p, int d, int heads_per_tile, bool final_out,
+                      hipStream_t s) {
+  if (p.n_items == 0) return hipSuccess;
+  if (d == 64) return launch_fwd_d<64>(p, heads_per_tile, final_out, s);
+  if (d == 128) return launch_fwd_d<128>(p, heads_per_tile, final_out, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace fck

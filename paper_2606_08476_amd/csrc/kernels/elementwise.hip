@@ -1,0 +1,151 @@
+// Bandwidth-bound kernels: the KV gather (simulated receive), the
+// log-sum-exp merge of two partial passes, and the backward preprocess.
+// Each moves whole rows with 16-byte accesses, consecutive lanes on
+// consecutive addresses.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace fck {
+
+// Row copies: output row i of K/V local (i < t_q) or received (i >= t_q)
+// comes from packed row q_gpos[i] or recv_gpos[i - t_q].
+__global__ __launch_bounds__(256) void kv_gather_kernel(const uint4* __restrict__ k,
+                                                        const uint4* __restrict__ v,
+                                                        const int32_t* __restrict__ q_gpos,
+                                                        const int32_t* __restrict__ recv_gpos,
+                                                        int32_t t_q, int32_t t_r, int32_t chunks,
+                                                        uint4* k_loc, uint4* v_loc, uint4* k_recv,
+                                                        uint4* v_recv) {
+  const int64_t total = int64_t(t_q + t_r) * chunks;
+  for (int64_t c = int64_t(blockIdx.x) * 256 + threadIdx.x; c < total;
+       c += int64_t(gridDim.x) * 256) {
+    const int32_t row = int32_t(c / chunks), cc = int32_t(c % chunks);
+    const bool loc = row < t_q;
+    const int64_t src = int64_t(loc ? q_gpos[row] : recv_gpos[row - t_q]) * chunks + cc;
+    const int64_t dst = int64_t(loc ? row : row - t_q) * chunks + cc;
+    const uint4 kk = k[src], vv = v[src];
+    (loc ? k_loc : k_recv)[dst] = kk;
+    (loc ? v_loc : v_recv)[dst] = vv;
+  }
+}
+
+// One (token, head) row per LPR lanes; each lane handles 4 values.
+template <int D>
+__global__ __launch_bounds__(256) void lse_merge_kernel(const float* __restrict__ oa,
+                                                        const float* __restrict__ la,
+                                                        const float* __restrict__ ob,
+                                                        const float* __restrict__ lb, int32_t t,
+                                                        int32_t h, u16* o, float* of,
+                                                        float* lse_out) {
+  constexpr int LPR = D / 4;
+  const int64_t row = (int64_t(blockIdx.x) * 256 + threadIdx.x) / LPR;
+  const int c = threadIdx.x % LPR;
+  if (row >= int64_t(t) * h) return;
+  const int32_t tok = int32_t(row / h), head = int32_t(row % h);
+  const int64_t li = int64_t(head) * t + tok;
+  const float a = la[li], bb = lb[li];
+  const float mx = fmaxf(a, bb);
+  const float m = mx == -INFINITY ? 0.f : mx;
+  const float wa = __expf(a - m), wb = __expf(bb - m);
+  const float tot = wa + wb;
+  const float ca = wa / tot, cb = wb / tot;
+  const f32x4 x = reinterpret_cast<const f32x4*>(oa + row * D)[c];
+  const f32x4 y = reinterpret_cast<const f32x4*>(ob + row * D)[c];
+  f32x4 r;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) r[j] = ca * x[j] + cb * y[j];
+  uint2 pk;
+  pk.x = uint32_t(f2bf(r[0])) | (uint32_t(f2bf(r[1])) << 16);
+  pk.y = uint32_t(f2bf(r[2])) | (uint32_t(f2bf(r[3])) << 16);
+  reinterpret_cast<uint2*>(o + row * D)[c] = pk;
+  if (of) reinterpret_cast<f32x4*>(of + row * D)[c] = r;
+  if (c == 0) lse_out[li] = m + __logf(tot);
+}
+
+// delta[head, tok] = sum_d dO * O over one (token, head) row; also zeroes
+// the row of dq, which the backward accumulates into.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_pre_kernel(const u16* __restrict__ o,
+                                                      const u16* __restrict__ dout,
+                                                      float* delta, float* dq, int32_t t,
+                                                      int32_t h) {
+  constexpr int LPR = D / 8;  // lanes per row, 8 values each
+  const int64_t row = (int64_t(blockIdx.x) * 256 + threadIdx.x) / LPR;
+  const int c = threadIdx.x % LPR;
+  const bool ok = row < int64_t(t) * h;
+  float acc = 0.f;
+  if (ok) {
+    const uint4 a = reinterpret_cast<const uint4*>(o + row * D)[c];
+    const uint4 g = reinterpret_cast<const uint4*>(dout + row * D)[c];
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, gw[4] = {g.x, g.y, g.z, g.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc += bf2f(u16(aw[j] & 0xffff)) * bf2f(u16(gw[j] & 0xffff));
+      acc += bf2f(u16(aw[j] >> 16)) * bf2f(u16(gw[j] >> 16));
+    }
+    f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    reinterpret_cast<f32x4*>(dq + row * D)[2 * c] = z;
+    reinterpret_cast<f32x4*>(dq + row * D)[2 * c + 1] = z;
+  }
+#pragma unroll
+  for (int w = LPR / 2; w >= 1; w >>= 1) acc += __shfl_xor(acc, w);
+  if (ok && c == 0) {
+    const int32_t tok = int32_t(row / h), head = int32_t(row % h);
+    delta[int64_t(head) * t + tok] = acc;
+  }
+}
+
+static unsigned grid_for(int64_t threads) {
+  const int64_t b = (threads + 255) / 256;
+  return unsigned(b < 1 ? 1 : b);
+}
+
+hipError_t launch_kv_gather(const uint16_t* k, const uint16_t* v, const int32_t* q_gpos,
+                            const int32_t* recv_gpos, int32_t t_q, int32_t t_r, int32_t row_elems,
+                            uint16_t* k_loc, uint16_t* v_loc, uint16_t* k_recv, uint16_t* v_recv,
+                            hipStream_t s) {
+  const int32_t chunks = row_elems / 8;
+  const int64_t total = int64_t(t_q + t_r) * chunks;
+  if (total == 0) return hipSuccess;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 256 * 64) blocks = 256 * 64;
+  hipLaunchKernelGGL(kv_gather_kernel, dim3(unsigned(blocks)), dim3(256), 0, s,
+                     reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v), q_gpos,
+                     recv_gpos, t_q, t_r, chunks, reinterpret_cast<uint4*>(k_loc),
+                     reinterpret_cast<uint4*>(v_loc), reinterpret_cast<uint4*>(k_recv),
+                     reinterpret_cast<uint4*>(v_recv));
+  return hipGetLastError();
+}
+
+hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o_b,
+                            const float* lse_b, int32_t t, int32_t h, int32_t d, uint16_t* o_bf16,
+                            float* o_f32, float* lse_out, hipStream_t s) {
+  const int64_t rows = int64_t(t) * h;
+  if (rows == 0) return hipSuccess;
+  if (d == 64)
+    hipLaunchKernelGGL(lse_merge_kernel<64>, dim3(grid_for(rows * 16)), dim3(256), 0, s, o_a, lse_a,
+                       o_b, lse_b, t, h, o_bf16, o_f32, lse_out);
+  else if (d == 128)
+    hipLaunchKernelGGL(lse_merge_kernel<128>, dim3(grid_for(rows * 32)), dim3(256), 0, s, o_a,
+                       lse_a, o_b, lse_b, t, h, o_bf16, o_f32, lse_out);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta, float* dq,
+                                 int32_t t, int32_t h, int32_t d, hipStream_t s) {
+  const int64_t rows = int64_t(t) * h;
+  if (rows == 0) return hipSuccess;
+  if (d == 64)
+    hipLaunchKernelGGL(bwd_pre_kernel<64>, dim3(grid_for(rows * 8)), dim3(256), 0, s, o, dout,
+                       delta, dq, t, h);
+  else if (d == 128)
+    hipLaunchKernelGGL(bwd_pre_kernel<128>, dim3(grid_for(rows * 16)), dim3(256), 0, s, o, dout,
+                       delta, dq, t, h);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace fck

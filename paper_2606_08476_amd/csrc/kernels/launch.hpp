@@ -1,0 +1,64 @@
+// Kernel parameter blocks and host-side launchers (implemented in the .hip
+// files). Only the C ABI layer calls these, after validating everything.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fck {
+
+struct FwdParams {
+  const uint16_t* q;        // [t_q, hq, d] bf16
+  const uint16_t* k_recv;   // [t_r, hkv, d]
+  const uint16_t* v_recv;
+  const uint16_t* k_loc;    // [t_q, hkv, d]
+  const uint16_t* v_loc;
+  const int32_t* items;     // 8 int32 per item: q0 q1 r0 r1 l0 l1 ldiag seg
+  const int32_t* perm;      // launch order
+  int32_t n_items;
+  int32_t hq, hkv, group, head_chunks;
+  float scale_log2;         // softmax scale * log2(e)
+  // outputs; final: o_bf16 (+ o_f32 if non-null) + lse; partial: o_f32 + lse
+  uint16_t* o_bf16;
+  float* o_f32;
+  float* lse;               // [hq, t_q]
+  int32_t t_q;
+};
+
+struct BwdParams {
+  const uint16_t* q;        // [t_q, hq, d]
+  const uint16_t* dout;     // [t_q, hq, d]
+  const float* lse;         // [hq, t_q] natural log
+  const float* delta;       // [hq, t_q] rowsum(dO * O)
+  const uint16_t* k_loc;
+  const uint16_t* v_loc;
+  const uint16_t* k_recv;
+  const uint16_t* v_recv;
+  const int32_t* items;     // 8 int32 per item: k0 k1 q0 q1 qfull src seg 0
+  const int32_t* perm;
+  const int32_t* lim;       // [t_q] receive index end per query
+  int32_t n_items;
+  int32_t hq, hkv, group;
+  float scale;
+  float* dq;                // [t_q, hq, d] fp32, accumulated atomically
+  float* dk_loc;            // [t_q, hkv, d] fp32
+  float* dv_loc;
+  float* dk_recv;           // [t_r, hkv, d] fp32
+  float* dv_recv;
+  int32_t t_q;
+};
+
+hipError_t launch_fwd(const FwdParams& p, int d, int heads_per_tile, bool final_out,
+                      hipStream_t s);
+hipError_t launch_bwd(const BwdParams& p, int d, hipStream_t s);
+hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta, float* dq,
+                                 int32_t t, int32_t h, int32_t d, hipStream_t s);
+hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o_b,
+                            const float* lse_b, int32_t t, int32_t h, int32_t d, uint16_t* o_bf16,
+                            float* o_f32, float* lse_out, hipStream_t s);
+hipError_t launch_kv_gather(const uint16_t* k, const uint16_t* v, const int32_t* q_gpos,
+                            const int32_t* recv_gpos, int32_t t_q, int32_t t_r, int32_t row_elems,
+                            uint16_t* k_loc, uint16_t* v_loc, uint16_t* k_recv, uint16_t* v_recv,
+                            hipStream_t s);
+
+}  // namespace fck

@@ -1,0 +1,221 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 CPU
+oracle on the same bf16 inputs.
+
+Tolerances: O (bf16 output) and dQ/dK/dV (fp32 outputs) max-abs <= 2e-2;
+LSE |err| <= 1e-3 * max(1, |LSE|); the gather and every integer table are
+bit-exact. Partial passes must reproduce -inf LSE and zero O on rows that
+see no key of their source.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import _cases
+from oracle import attention as A
+from paper_2606_08476_amd import flashcp as F
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 2e-2
+G_TOL = 2e-2
+LSE_TOL = 1e-3
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="session")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    F.lib()
+    return torch.device("cuda:0")
+
+
+def _lse_ok(got, ref):
+    got = got.double().cpu()
+    ref = ref.double()
+    fin = torch.isfinite(ref)
+    assert torch.equal(torch.isfinite(got), fin), "LSE -inf pattern differs"
+    assert torch.all(got[~fin] == ref[~fin])
+    err = (got[fin] - ref[fin]).abs() / ref[fin].abs().clamp_min(1.0)
+    return float(err.max()) if err.numel() else 0.0
+
+
+def _maxabs(a, b):
+    return float((a.double().cpu() - b.double()).abs().max()) if a.numel() else 0.0
+
+
+class Run:
+    """One case on the GPU: view, gathered KV, forward and backward outputs."""
+
+    def __init__(self, case, dev, mode=F.FC_TWO_PASS, x=None):
+        self.case = case
+        say(f"[gpu] case={case.name} rank={case.rank} heads={case.hq}/{case.hkv} d={case.d} mode={mode}")
+        self.x = _cases.inputs(case) if x is None else x
+        x = {k: v.to(dev) for k, v in self.x.items()}
+        self.v = F.View(case.cu, case.plan, case.cp, case.rank, case.hq, case.hkv, case.d).bind(dev)
+        i = self.v.info
+        tq, tr, hq, hkv, d = i["t_q"], i["t_recv"], i["hq"], i["hkv"], i["d"]
+        bf = torch.bfloat16
+        self.k_loc = torch.empty(tq, hkv, d, dtype=bf, device=dev)
+        self.v_loc = torch.empty_like(self.k_loc)
+        self.k_recv = torch.empty(tr, hkv, d, dtype=bf, device=dev)
+        self.v_recv = torch.empty_like(self.k_recv)
+        F.fc_kv_gather(self.v, x["k_pk"], x["v_pk"], self.k_loc, self.v_loc, self.k_recv, self.v_recv)
+        self.q, self.do = x["q"], x["do"]
+        self.o = torch.empty(tq, hq, d, dtype=bf, device=dev)
+        self.o32 = torch.empty(tq, hq, d, dtype=torch.float32, device=dev)
+        self.lse = torch.empty(hq, tq, dtype=torch.float32, device=dev)
+        fws, bws = self.v.workspace_size(mode)
+        ws = torch.empty(max(fws, 1), dtype=torch.uint8, device=dev)
+        F.fc_attn_fwd(self.v, self.q, self.k_loc, self.v_loc, self.k_recv, self.v_recv, 0.0, mode,
+                      self.o, self.o32, self.lse, ws)
+        f32 = torch.float32
+        self.dq = torch.empty(tq, hq, d, dtype=f32, device=dev)
+        self.dk_loc = torch.empty(tq, hkv, d, dtype=f32, device=dev)
+        self.dv_loc = torch.empty_like(self.dk_loc)
+        self.dk_recv = torch.empty(tr, hkv, d, dtype=f32, device=dev)
+        self.dv_recv = torch.empty_like(self.dk_recv)
+        bws_t = torch.empty(bws, dtype=torch.uint8, device=dev)
+        F.fc_attn_bwd(self.v, self.q, self.k_loc, self.v_loc, self.k_recv, self.v_recv, self.o,
+                      self.lse, self.do, 0.0, self.dq, self.dk_loc, self.dv_loc, self.dk_recv,
+                      self.dv_recv, bws_t)
+        torch.cuda.synchronize()
+        say(f"[gpu] case={case.name} done")
+
+    def oracle_fwd(self, rows=None):
+        c, o, x = self.case, self.case.oview, self.x
+        kv = np.concatenate([o.q_gpos, o.recv_gpos])
+        k = torch.cat([x["k_loc"], x["k_recv"]])
+        v = torch.cat([x["v_loc"], x["v_recv"]])
+        return A.attention_fwd(c.cu, o.q_gpos, x["q"], kv, k, v, rows=rows)
+
+    def oracle_bwd(self, rows=None):
+        c, o, x = self.case, self.case.oview, self.x
+        kv = np.concatenate([o.q_gpos, o.recv_gpos])
+        k = torch.cat([x["k_loc"], x["k_recv"]])
+        v = torch.cat([x["v_loc"], x["v_recv"]])
+        return A.attention_bwd(c.cu, o.q_gpos, x["q"], kv, k, v, x["do"], rows=rows)
+
+
+_RUNS = {}
+
+
+def get_run(key, dev, mode=F.FC_TWO_PASS):
+    if (key, mode) not in _RUNS:
+        _RUNS[(key, mode)] = Run(_cases.small_case(key), dev, mode)
+    return _RUNS[(key, mode)]
+
+
+SMALL = list(_cases.SMALL)
+
+
+@pytest.mark.parametrize("key", SMALL)
+def test_gather_is_exact(key, dev):
+    r = get_run(key, dev)
+    assert torch.equal(r.k_loc.cpu(), r.x["k_loc"]) and torch.equal(r.v_loc.cpu(), r.x["v_loc"])
+    assert torch.equal(r.k_recv.cpu(), r.x["k_recv"]) and torch.equal(r.v_recv.cpu(), r.x["v_recv"])
+
+
+@pytest.mark.parametrize("key", SMALL)
+def test_forward_two_pass(key, dev):
+    r = get_run(key, dev)
+    O, L = r.oracle_fwd()
+    eo = _maxabs(r.o, O)
+    eo32 = _maxabs(r.o32, O)
+    el = _lse_ok(r.lse, L)
+    say(f"[gpu] {key} fwd two-pass: O bf16 {eo:.3e} O fp32 {eo32:.3e} LSE {el:.3e}")
+    assert eo <= O_TOL and eo32 <= O_TOL and el <= LSE_TOL
+
+
+@pytest.mark.parametrize("key", SMALL)
+def test_forward_fused(key, dev):
+    r = get_run(key, dev, F.FC_FUSED)
+    O, L = r.oracle_fwd()
+    eo, el = _maxabs(r.o, O), _lse_ok(r.lse, L)
+    say(f"[gpu] {key} fwd fused: O {eo:.3e} LSE {el:.3e}")
+    assert eo <= O_TOL and el <= LSE_TOL
+
+
+@pytest.mark.parametrize("key", SMALL)
+def test_partial_passes_and_merge(key, dev):
+    r = get_run(key, dev)
+    c, o, x = r.case, r.case.oview, r.x
+    i = r.v.info
+    tq, hq, d = i["t_q"], i["hq"], i["d"]
+    outs = []
+    for src, kg, vg, keys in ((0, r.k_loc, r.v_loc, o.q_gpos), (1, r.k_recv, r.v_recv, o.recv_gpos)):
+        op = torch.empty(tq, hq, d, dtype=torch.float32, device=dev)
+        lp = torch.empty(hq, tq, dtype=torch.float32, device=dev)
+        F.fc_attn_fwd_partial(r.v, src, r.q, kg, vg, 0.0, op, lp)
+        kk = x["k_loc"] if src == 0 else x["k_recv"]
+        vv = x["v_loc"] if src == 0 else x["v_recv"]
+        Oref, Lref = A.attention_fwd(c.cu, o.q_gpos, x["q"], keys, kk, vv)
+        torch.cuda.synchronize()
+        eo, el = _maxabs(op, Oref), _lse_ok(lp, Lref)
+        say(f"[gpu] {key} partial src={src}: O {eo:.3e} LSE {el:.3e}")
+        assert eo <= O_TOL and el <= LSE_TOL
+        outs.append((Oref, Lref))
+    # the merge kernel on the oracle's partials against the oracle's merge
+    (Oa, La), (Ob, Lb) = outs
+    Om, Lm = A.lse_merge(Oa, La, Ob, Lb)
+    dv = lambda t: t.float().contiguous().to(dev)
+    ob = torch.empty(tq, hq, d, dtype=torch.bfloat16, device=dev)
+    of = torch.empty(tq, hq, d, dtype=torch.float32, device=dev)
+    lo = torch.empty(hq, tq, dtype=torch.float32, device=dev)
+    F.fc_lse_merge(dv(Oa), dv(La), dv(Ob), dv(Lb), ob, of, lo)
+    torch.cuda.synchronize()
+    assert _maxabs(ob, Om) <= O_TOL and _maxabs(of, Om) <= 1e-5 and _lse_ok(lo, Lm) <= 1e-5
+
+
+@pytest.mark.parametrize("key", SMALL)
+def test_backward(key, dev):
+    r = get_run(key, dev)
+    dq, dk, dv = r.oracle_bwd()
+    tq = r.v.info["t_q"]
+    e = dict(dq=_maxabs(r.dq, dq), dk_loc=_maxabs(r.dk_loc, dk[:tq]), dv_loc=_maxabs(r.dv_loc, dv[:tq]),
+             dk_recv=_maxabs(r.dk_recv, dk[tq:]), dv_recv=_maxabs(r.dv_recv, dv[tq:]))
+    say(f"[gpu] {key} bwd: " + " ".join(f"{k} {v:.3e}" for k, v in e.items()))
+    assert max(e.values()) <= G_TOL, e
+
+
+def test_document_isolation_on_gpu(dev):
+    """Changing one document's Q/K/V/dO leaves every other document's GPU
+    outputs bit-identical (dQ, accumulated with atomics, to rounding)."""
+    case = _cases.small_case("llama8b_8k")
+    x = _cases.inputs(case)
+    base = Run(case, dev, x=x)
+    o = case.oview
+    seg = 1
+    s0, s1 = int(o.q_cu_docseg[seg]), int(o.q_cu_docseg[seg + 1])
+    r0, r1 = int(o.recv_cu[seg]), int(o.recv_cu[seg + 1])
+    doc = int(o.seg_doc[seg])
+    lo, hi = int(case.cu[doc]), int(case.cu[doc + 1])
+    x2 = {k: v.clone() for k, v in x.items()}
+    for name in ("k_pk", "v_pk"):
+        x2[name][lo:hi] = (x2[name][lo:hi].float() * -1.25 + 0.5).to(torch.bfloat16)
+    for name in ("q", "do"):
+        x2[name][s0:s1] = (x2[name][s0:s1].float() * 0.75 - 0.1).to(torch.bfloat16)
+    pert = Run(case, dev, x=x2)
+    keep = np.r_[0:s0, s1:o.q_gpos.size]
+    keep_r = np.r_[0:r0, r1:o.recv_gpos.size]
+    for n in ("o", "dk_loc", "dv_loc"):
+        assert torch.equal(getattr(pert, n)[keep].cpu(), getattr(base, n)[keep].cpu()), n
+    assert torch.equal(pert.lse[:, keep].cpu(), base.lse[:, keep].cpu())
+    for n in ("dk_recv", "dv_recv"):
+        assert torch.equal(getattr(pert, n)[keep_r].cpu(), getattr(base, n)[keep_r].cpu()), n
+    assert _maxabs(pert.dq[keep], base.dq[keep].cpu().double()) <= 1e-5
+    assert not torch.equal(pert.o[s0:s1].cpu(), base.o[s0:s1].cpu())
+
+
+def test_repeat_runs_deterministic(dev):
+    """Forward outputs and dK/dV (no atomics) are bit-identical across runs."""
+    a = Run(_cases.small_case("longdoc_16k"), dev)
+    b = Run(_cases.small_case("longdoc_16k"), dev)
+    for n in ("o", "lse", "dk_loc", "dv_loc", "dk_recv", "dv_recv"):
+        assert torch.equal(getattr(a, n), getattr(b, n)), n
+    assert _maxabs(a.dq, b.dq.cpu().double()) <= 1e-5

@@ -1,0 +1,194 @@
+"""Host side of the C ABI, no GPU: the library loads and exports every
+function the header declares; planners, rank views and tile maps are
+bit-exact with the oracle; invalid input is rejected with its error code
+before anything is launched."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import planner as P
+from oracle import view as V
+from paper_2606_08476_amd import flashcp as F
+from paper_2606_08476_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flashcp.h")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built():
+    if not os.path.exists(F._LIB_PATH):
+        from paper_2606_08476_amd import build
+        build.build()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fc_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = _declared()
+    assert len(names) >= 16
+    lib = C.CDLL(F._LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(F.EXPORTS) == names
+
+
+def _cu(lens):
+    return np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+
+
+def _random_cases(n=25, seed=7):
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        N = int(rng.choice([1, 2, 3, 4, 8]))
+        k = int(rng.integers(1, 14))
+        lens = [int(x) for x in rng.integers(1, 500, size=k)]
+        lens[-1] += (-sum(lens)) % N
+        yield _cu(lens), N
+
+
+def test_planners_bit_exact_random():
+    for cu, N in _random_cases():
+        assert np.array_equal(F.fc_plan_per_doc(cu, N), P.plan_per_doc(cu, N))
+        assert np.array_equal(F.fc_plan_whole_lpt(cu, N), P.plan_whole_lpt(cu, N))
+        for R in (1.0, 1.05, 1.3):
+            a, ia = F.fc_plan_hybrid(cu, N, R)
+            b, ib = P.plan_hybrid(cu, N, R)
+            assert np.array_equal(a, b) and np.array_equal(ia, ib)
+            assert F.fc_plan_stats(cu, N, a, 2, 64) == P.stats(cu, N, b, 2, 64)
+
+
+@pytest.mark.parametrize("name", list(synth.WORKLOADS))
+def test_planners_bit_exact_workloads(name):
+    w = synth.WORKLOADS[name]
+    cu = synth.cu_seqlens(synth.doc_lengths(name))
+    assert np.array_equal(F.fc_plan_per_doc(cu, w.cp), P.plan_per_doc(cu, w.cp))
+    assert np.array_equal(F.fc_plan_whole_lpt(cu, w.cp), P.plan_whole_lpt(cu, w.cp))
+    a, ia = F.fc_plan_hybrid(cu, w.cp)
+    b, ib = P.plan_hybrid(cu, w.cp)
+    assert np.array_equal(a, b) and np.array_equal(ia, ib)
+    for plan in (a, F.fc_plan_per_doc(cu, w.cp), F.fc_plan_whole_lpt(cu, w.cp)):
+        assert F.fc_plan_stats(cu, w.cp, plan, w.hkv, w.d) == P.stats(cu, w.cp, plan, w.hkv, w.d)
+
+
+def _compare_view(cu, plan, N, r, hq, hkv, d):
+    v = F.View(cu, plan, N, r, hq, hkv, d)
+    e = v.export()
+    o = V.rank_view(cu, plan, r)
+    i = v.info
+    assert np.array_equal(e["q_gpos"], o.q_gpos)
+    assert np.array_equal(e["recv_gpos"], o.recv_gpos)
+    assert np.array_equal(e["seg_doc"], o.seg_doc)
+    assert np.array_equal(e["q_cu_docseg"], o.q_cu_docseg)
+    assert np.array_equal(e["recv_cu"], o.recv_cu)
+    assert np.array_equal(e["pieces"], o.pieces)
+    assert np.array_equal(e["lim"], o.lim)
+    assert (i["pairs_loc"], i["pairs_recv"]) == (o.pairs_loc, o.pairs_recv)
+    for mode in ("local", "recv", "fused"):
+        assert np.array_equal(e["fwd_" + mode], V.fwd_items(o, i["bm_fwd"], i["bn_fwd"], mode)), mode
+    assert np.array_equal(e["bwd"], V.bwd_items(o, i["bm_bwd"], i["bn_bwd"]))
+    v.close()
+
+
+def test_views_bit_exact_random():
+    for cu, N in _random_cases(12, seed=9):
+        for plan in (P.plan_per_doc(cu, N), P.plan_hybrid(cu, N)[0]):
+            for r in range(N):
+                for hq, hkv, d in ((4, 4, 64), (8, 2, 128), (16, 2, 128)):
+                    _compare_view(cu, plan, N, r, hq, hkv, d)
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b", "wholedoc"])
+def test_views_bit_exact_workload_ranks(name):
+    w = synth.WORKLOADS[name]
+    cu = synth.cu_seqlens(synth.doc_lengths(name))
+    plan = {"per_doc": P.plan_per_doc, "whole_lpt": P.plan_whole_lpt}[w.plan](cu, w.cp)
+    ranks = [0, w.cp - 1] if name != "tiny" else [0, 1]
+    for r in ranks:
+        _compare_view(cu, plan, w.cp, r, w.hq, w.hkv, w.d)
+
+
+def test_heaviest_rank_agrees():
+    """The rank the workloads name as heaviest (argmax W, lowest on ties)
+    is the same from the C ABI and the oracle."""
+    for name in ("wholedoc", "hybrid70b"):
+        w = synth.WORKLOADS[name]
+        cu = synth.cu_seqlens(synth.doc_lengths(name))
+        plan = F.fc_plan_whole_lpt(cu, w.cp) if w.plan == "whole_lpt" else F.fc_plan_hybrid(cu, w.cp)[0]
+        a = F.fc_plan_stats(cu, w.cp, plan, w.hkv, w.d)["work"]
+        b = P.stats(cu, w.cp, plan, w.hkv, w.d)["work"]
+        assert a == b and int(np.argmax(a)) == int(np.argmax(b))
+
+
+def _code(fn, *a):
+    with pytest.raises(F.FlashCPError) as ei:
+        fn(*a)
+    return ei.value.code
+
+
+def test_error_codes():
+    cu = _cu([5, 3])
+    ok = np.array([[0, 0, 0, 5], [1, 1, 0, 3]], dtype=np.int32)
+    F.fc_plan_validate(cu, 2, ok)
+    assert _code(F.fc_plan_validate, cu, 2, np.array([[0, 0, 0, 4], [1, 1, 0, 3]])) == -2   # gap
+    assert _code(F.fc_plan_validate, cu, 2,
+                 np.array([[0, 0, 0, 5], [0, 1, 4, 1], [1, 1, 0, 3]])) == -2               # overlap
+    assert _code(F.fc_plan_validate, cu, 2, np.array([[0, 0, 0, 6], [1, 1, 0, 3]])) == -2   # beyond doc
+    assert _code(F.fc_plan_validate, cu, 2, np.array([[0, 2, 0, 5], [1, 1, 0, 3]])) == -2   # rank >= N
+    assert _code(F.fc_plan_validate, cu, 2, ok, True) == -2                                 # Eq. 2
+    assert _code(F.fc_plan_per_doc, np.array([0, 4, 4], dtype=np.int32), 2) == -1           # empty doc
+    assert _code(F.fc_plan_per_doc, cu, 0) == -1
+    assert _code(F.fc_plan_hybrid, _cu([5, 2]), 2) == -1                                    # N does not divide C
+    assert _code(F.View, cu, ok, 2, 0, 6, 4, 64) == -1                                       # hq % hkv
+    assert _code(F.View, cu, ok, 2, 0, 4, 4, 96) == -4                                       # head dim
+    assert _code(F.View, cu, ok, 2, 0, 12, 4, 64) == -4                                      # group of 3
+    assert _code(F.View, cu, ok, 2, 2, 4, 4, 64) == -1                                       # rank
+    assert _code(F.View, cu, np.array([[0, 0, 0, 4], [1, 1, 0, 3]]), 2, 0, 4, 4, 64) == -2  # bad plan
+    # capacity: n_out reports the need
+    lib = F.lib()
+    n = C.c_int64(0)
+    buf = (F.Shard * 1)()
+    rc = lib.fc_plan_per_doc(cu.ctypes.data_as(F.I32P), 2, 2, buf, 1, C.byref(n))
+    assert rc == -7 and n.value == len(P.plan_per_doc(cu, 2))
+    assert lib.fc_plan_per_doc(None, 2, 2, buf, 1, C.byref(n)) == -1
+
+
+def test_kernel_calls_rejected_before_launch():
+    """Device entry points refuse an unbound view, bad modes and bad
+    workspaces on the host: no GPU is touched."""
+    lib = F.lib()
+    cu = _cu([64, 64])
+    plan = P.plan_per_doc(cu, 2)
+    v = F.View(cu, plan, 2, 0, 4, 4, 64)
+    h = v.handle
+    assert lib.fc_kv_gather(h, 1, 1, 128, 1, 1, 1, 1, None) == -5
+    assert lib.fc_attn_fwd(h, 1, 1, 1, 1, 1, 0.0, 0, 1, None, 1, None, 0, None) == -5
+    assert lib.fc_attn_bwd(h, *([1] * 8), 0.0, *([1] * 5), None, 0, None) == -5
+    assert lib.fc_attn_fwd_partial(h, 0, 1, 1, 1, 0.0, 1, 1, None) == -5
+    assert lib.fc_lse_merge(1, 1, 1, 1, 4, 2, 96, 1, None, 1, None) == -4
+    assert lib.fc_lse_merge(1, 1, 1, 1, -1, 2, 64, 1, None, 1, None) == -1
+    f, b = v.workspace_size(F.FC_TWO_PASS)
+    i = v.info
+    assert f == 2 * (i["t_q"] * 4 * 64 * 4 + ((i["t_q"] * 4 * 4 + 255) // 256) * 256)
+    assert v.workspace_size(F.FC_FUSED)[0] == 0
+    assert lib.fc_workspace_size(h, 7, None, None) == -1
+    assert lib.fc_view_bind(h, None, 0, None) == -1
+    assert lib.fc_view_bind(h, 256, 4, None) == -5       # too small, rejected before any copy
+    assert lib.fc_view_bind(h, 257, 1 << 20, None) == -1  # misaligned
+    v.close()
+
+
+def test_empty_rank_view():
+    """A rank with no shards has an empty view; its calls are no-ops."""
+    cu = _cu([10])
+    plan = np.array([[0, 0, 0, 10]], dtype=np.int32)
+    v = F.View(cu, plan, 2, 1, 4, 4, 64)
+    assert v.info["t_q"] == 0 and v.info["t_recv"] == 0 and v.info["n_bwd"] == 0
+    v.close()

@@ -177,3 +177,20 @@ def test_empty_partial_pass():
     assert torch.isinf(L[:, :5]).all() and (L[:, :5] < 0).all()
     assert torch.all(O[:5] == 0)
     assert torch.isinf(L[:, 5:]).logical_not().all()
+
+
+def test_row_restricted_backward_is_exact_for_its_documents():
+    """Restricting the backward to the queries of some documents gives the
+    full dQ on those rows and the full dK/dV on those documents' keys."""
+    lens = [17, 30, 9]
+    cu, q, k, v, do = _packed(lens, 4, 2, 8, 10)
+    T = cu[-1]
+    ar = np.arange(T)
+    dq, dk, dv = A.attention_bwd(cu, ar, q, ar, k, v, do, 0.3)
+    rows = np.arange(cu[1], cu[2])
+    dq2, dk2, dv2 = A.attention_bwd(cu, ar, q, ar, k, v, do, 0.3, rows=rows)
+    assert torch.allclose(dq2[rows], dq[rows], atol=1e-14)
+    assert torch.allclose(dk2[rows], dk[rows], atol=1e-14)
+    assert torch.allclose(dv2[rows], dv[rows], atol=1e-14)
+    other = np.setdiff1d(ar, rows)
+    assert torch.all(dq2[other] == 0) and torch.all(dk2[other] == 0)
