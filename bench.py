@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Throughput of one context-parallel rank's share of FlashCP's attention
+(forward + backward) on one MI355X.
+
+A step is the whole path once over one synthetic packed sequence: the shard
+plan and rank view (host, C++), the table upload, the KV gather that stands
+in for the sharding-aware receive, the local and received forward passes,
+their log-sum-exp merge, the backward preprocess and the key-major backward.
+Inputs are resident in HBM before timing starts. The metric counts useful
+FLOPs: 14 * d * Hq * pairs, pairs being the visible (query, key) pairs per
+head of the rank (sum of its shards' W_i); masked lanes never count.
+
+Prints one JSON line. Only one GPU is supported.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "useful attention TFLOP/s (fwd+bwd) per CP-rank shard; % of bf16 MFMA peak"
+BF16_PEAK_TFLOPS = 2516.6   # 256 CUs x 2.4 GHz x 4096 bf16 flop/clk/CU (dense)
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama8b")
+    ap.add_argument("--mode", choices=["two_pass"], default="two_pass")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the CPU-oracle baseline sample (0 disables it)")
+    return ap.parse_args()
+
+
+def plan_for(F, w, cu):
+    if w.plan == "per_doc":
+        return F.fc_plan_per_doc(cu, w.cp)
+    if w.plan == "whole_lpt":
+        return F.fc_plan_whole_lpt(cu, w.cp)
+    return F.fc_plan_hybrid(cu, w.cp)[0]
+
+
+def rank_for(F, w, cu, plan):
+    if w.rank == "last":
+        return w.cp - 1
+    if w.rank == "heaviest":
+        work = F.fc_plan_stats(cu, w.cp, plan, w.hkv, w.d)["work"]
+        return int(np.argmax(work))
+    return int(w.rank)
+
+
+def cpu_baseline(cu, view_tables, x, w, seconds):
+    """The oracle (fp32, as it stands) on whole document segments of the
+    rank, forward + backward, until the time budget is used."""
+    import torch
+    from oracle import attention as A
+    qg, rg = view_tables["q_gpos"].astype(np.int64), view_tables["recv_gpos"].astype(np.int64)
+    qcu = view_tables["q_cu_docseg"]
+    rcu = view_tables["recv_cu"]
+    kv = np.concatenate([qg, rg])
+    k = torch.cat([x["k_loc"], x["k_recv"]])
+    v = torch.cat([x["v_loc"], x["v_recv"]])
+    torch.set_num_threads(max(1, min(os.cpu_count() or 1, int(os.environ.get("OMP_NUM_THREADS", "16")))))
+    # smallest segments first, so the sample finishes within the budget
+    segs = sorted(range(len(qcu) - 1), key=lambda s: int(qcu[s + 1] - qcu[s]) * int(rcu[s + 1] - rcu[s] + qcu[s + 1] - qcu[s]))
+    pairs = 0
+    done = 0
+    t0 = time.perf_counter()
+    for s in segs:
+        rows = np.arange(qcu[s], qcu[s + 1])
+        A.attention_fwd(cu, qg, x["q"], kv, k, v, rows=rows, dtype=torch.float32)
+        A.attention_bwd(cu, qg, x["q"], kv, k, v, x["do"], rows=rows, dtype=torch.float32)
+        n = int(rows.size)
+        # pairs of this segment: local causal + received prefix per row
+        lim = view_tables["lim"][rows] - rcu[s]
+        pairs += n * (n + 1) // 2 + int(lim.sum())
+        done += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    flops = 14.0 * w.d * w.hq * pairs
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"{done} of {len(segs)} document segments of the same rank share (smallest first), "
+                      f"{pairs} pairs/head = {100.0 * pairs / max(1, view_tables['pairs']):.2f}% of the "
+                      f"rank's work, forward + backward in fp32, {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs one rank's share on one GPU; --gpus must be 1 "
+              "(multi-GPU exchange is not part of it)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_08476_amd import flashcp as F
+    from paper_2606_08476_amd import synth
+
+    w = synth.WORKLOADS[args.workload]
+    lens = synth.doc_lengths(args.workload)
+    cu = synth.cu_seqlens(lens)
+    dev = torch.device("cuda:0")
+    plan = plan_for(F, w, cu)
+    rank = rank_for(F, w, cu, plan)
+    view = F.View(cu, plan, w.cp, rank, w.hq, w.hkv, w.d)
+    info = view.info
+    tab = view.export()
+    tq, tr, hq, hkv, d = info["t_q"], info["t_recv"], w.hq, w.hkv, w.d
+    pairs = info["pairs_loc"] + info["pairs_recv"]
+    tab["pairs"] = pairs
+
+    # inputs, resident in HBM before timing
+    src = synth.TensorSource(w.index, hq, hkv, d)
+    qg, rg = tab["q_gpos"], tab["recv_gpos"]
+    x = {"q": src.rows("q", qg), "do": src.rows("do", qg), "k_loc": src.rows("k", qg),
+         "v_loc": src.rows("v", qg), "k_recv": src.rows("k", rg), "v_recv": src.rows("v", rg)}
+    T = int(cu[-1])
+    bf, f32 = torch.bfloat16, torch.float32
+    k_pk = torch.zeros(T, hkv, d, dtype=bf, device=dev)
+    v_pk = torch.zeros(T, hkv, d, dtype=bf, device=dev)
+    k_pk[torch.from_numpy(qg.astype(np.int64)).to(dev)] = x["k_loc"].to(dev)
+    v_pk[torch.from_numpy(qg.astype(np.int64)).to(dev)] = x["v_loc"].to(dev)
+    if tr:
+        k_pk[torch.from_numpy(rg.astype(np.int64)).to(dev)] = x["k_recv"].to(dev)
+        v_pk[torch.from_numpy(rg.astype(np.int64)).to(dev)] = x["v_recv"].to(dev)
+    q = x["q"].to(dev)
+    do = x["do"].to(dev)
+    k_loc = torch.empty(tq, hkv, d, dtype=bf, device=dev)
+    v_loc = torch.empty_like(k_loc)
+    k_recv = torch.empty(tr, hkv, d, dtype=bf, device=dev)
+    v_recv = torch.empty_like(k_recv)
+    o_a = torch.empty(tq, hq, d, dtype=f32, device=dev)
+    o_b = torch.empty_like(o_a)
+    l_a = torch.empty(hq, tq, dtype=f32, device=dev)
+    l_b = torch.empty_like(l_a)
+    o = torch.empty(tq, hq, d, dtype=bf, device=dev)
+    lse = torch.empty(hq, tq, dtype=f32, device=dev)
+    delta = torch.empty(hq, tq, dtype=f32, device=dev)
+    dq = torch.empty(tq, hq, d, dtype=f32, device=dev)
+    dk_loc = torch.empty(tq, hkv, d, dtype=f32, device=dev)
+    dv_loc = torch.empty_like(dk_loc)
+    dk_recv = torch.empty(tr, hkv, d, dtype=f32, device=dev)
+    dv_recv = torch.empty_like(dk_recv)
+    meta = torch.empty(int(info["meta_bytes"]) + 256, dtype=torch.uint8, device=dev)
+    names = ["kv_gather", "attn_fwd_local", "attn_fwd_recv", "lse_merge", "bwd_preprocess", "attn_bwd"]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+    acc = np.zeros(len(names))
+    kept = []
+
+    def step(timed):
+        p = plan_for(F, w, cu)
+        v = F.View(cu, p, w.cp, rank, hq, hkv, d).bind(dev, meta)
+        kept.append(v)
+        ev[0].record()
+        F.fc_kv_gather(v, k_pk, v_pk, k_loc, v_loc, k_recv, v_recv)
+        ev[1].record()
+        F.fc_attn_fwd_partial(v, 0, q, k_loc, v_loc, 0.0, o_a, l_a)
+        ev[2].record()
+        if tr:
+            F.fc_attn_fwd_partial(v, 1, q, k_recv, v_recv, 0.0, o_b, l_b)
+            ev[3].record()
+            F.fc_lse_merge(o_a, l_a, o_b, l_b, o, None, lse)
+        else:
+            raise SystemExit("bench.py: workload has no received KV; two-pass mode needs it")
+        ev[4].record()
+        F.fc_bwd_preprocess(v, o, do, delta, dq)
+        ev[5].record()
+        F.fc_attn_bwd_pass(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq, dk_loc,
+                           dv_loc, dk_recv, dv_recv)
+        ev[6].record()
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    kept.clear()
+    t0 = time.perf_counter()
+    per = []
+    for _ in range(args.steps):
+        step(True)
+        # per-kernel durations are read after the loop from stored copies
+        per.append([ev[i] for i in range(len(ev))])
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    for e in per:
+        for i in range(len(names)):
+            acc[i] += e[i].elapsed_time(e[i + 1])
+    acc /= args.steps
+    for v in kept:
+        v.close()
+    kept.clear()
+
+    ms = wall * 1e3 / args.steps
+    useful = 14.0 * d * hq * pairs
+    value = useful / (ms * 1e-3) / 1e12
+    # per-kernel algorithmic work
+    kv_rows = tq + tr
+    work = {
+        "kv_gather": ("hbm", 2 * 2 * kv_rows * hkv * d * 2),
+        "attn_fwd_local": ("mfma", 4.0 * d * hq * info["pairs_loc"]),
+        "attn_fwd_recv": ("mfma", 4.0 * d * hq * info["pairs_recv"]),
+        "lse_merge": ("hbm", tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4)),
+        "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4 + 4 * d)),
+        "attn_bwd": ("mfma", 10.0 * d * hq * pairs),
+    }
+    kernels = {}
+    for i, n in enumerate(names):
+        kind, amount = work[n]
+        t = acc[i] * 1e-3
+        if kind == "mfma":
+            a = amount / t / 1e12
+            kernels[n] = {"ms": round(acc[i], 4), "tflops": round(a, 1), "frac_bf16_peak": round(a / BF16_PEAK_TFLOPS, 4)}
+        else:
+            a = amount / t / 1e9
+            kernels[n] = {"ms": round(acc[i], 4), "gbs": round(a, 1), "frac_hbm_peak": round(a / HBM_PEAK_GBS, 4)}
+    dom = max(range(len(names)), key=lambda i: acc[i])
+    dn = names[dom]
+    kind, amount = work[dn]
+    if kind == "mfma":
+        ach = amount / (acc[dom] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dn}
+    else:
+        ach = amount / (acc[dom] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dn}
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.context}-token packed context, CP degree {w.cp}, "
+                               f"{w.plan} plan, rank {rank}; {hq} query / {hkv} KV heads, d {d}; "
+                               "two-pass forward (local, received) + LSE merge, key-major backward",
+                   "t_q": tq, "t_recv": tr, "pairs_per_head": pairs,
+                   "useful_tflop_per_step": round(useful / 1e12, 4),
+                   "pct_of_bf16_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
+                   "strict_tflops_12d": round(12.0 * d * hq * pairs / (ms * 1e-3) / 1e12, 2)},
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(cu, tab, x, w, args.cpu_seconds)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

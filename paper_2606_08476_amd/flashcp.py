@@ -221,12 +221,16 @@ class View:
             out[k] = out[k].reshape(-1, 8)
         return out
 
-    def bind(self, device="cuda"):
-        """Allocate the device table buffer (torch) and upload on the current stream."""
+    def bind(self, device="cuda", buf=None):
+        """Upload the view's tables on the current stream into ``buf`` (a
+        uint8 device tensor, allocated here if not given) and keep it."""
         import torch
         nbytes = int(self.info["meta_bytes"])
-        buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        if buf is None:
+            buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
         off = (-buf.data_ptr()) % 256
+        if not buf.is_cuda or buf.numel() - off < nbytes:
+            raise ValueError("metadata buffer too small or not on the device")
         self.meta = buf
         _check(lib().fc_view_bind(self.handle, buf.data_ptr() + off, nbytes, _stream()))
         return self
