@@ -171,7 +171,7 @@ def main():
         else:
             raise SystemExit("bench.py: workload has no received KV; two-pass mode needs it")
         ev[4].record()
-        F.fc_bwd_preprocess(v, o, do, delta, dq)
+        F.fc_bwd_preprocess(v, o, do, delta)
         ev[5].record()
         F.fc_attn_bwd_pass(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq, dk_loc,
                            dv_loc, dk_recv, dv_recv)
@@ -208,7 +208,7 @@ def main():
         "attn_fwd_local": ("mfma", 4.0 * d * hq * info["pairs_loc"]),
         "attn_fwd_recv": ("mfma", 4.0 * d * hq * info["pairs_recv"]),
         "lse_merge": ("hbm", tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4)),
-        "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4 + 4 * d)),
+        "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4)),
         "attn_bwd": ("mfma", 10.0 * d * hq * pairs),
     }
     kernels = {}

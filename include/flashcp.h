@@ -214,7 +214,7 @@ int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const f
  * final (merged) lse, and dout. Writes dq (fp32 [T_q,Hq,d]), dk_loc/dv_loc
  * (fp32 [T_q,Hkv,d]) and dk_recv/dv_recv (fp32 [T_r,Hkv,d]); dK/dV are
  * summed over the query heads of each KV head. ws: device, >= bwd bytes.
- * dq is accumulated with atomics, so its rounding order is not fixed. */
+ * No atomics: results are bitwise reproducible for fixed inputs. */
 int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                 const void* k_recv, const void* v_recv, const void* o, const float* lse,
                 const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
@@ -222,9 +222,9 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
 
 /* The backward in its two steps (fc_attn_bwd runs both):
  * fc_bwd_preprocess writes delta[h, t] = sum_i dout[t,h,i] * o[t,h,i] (fp32
- * [Hq,T_q], device) and zeroes dq, which the pass accumulates into;
- * fc_attn_bwd_pass then computes dq, dk_*, dv_* from lse and delta. */
-int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta, float* dq,
+ * [Hq,T_q], device); fc_attn_bwd_pass then computes dk_*, dv_* (key-major
+ * kernel) and dq (query-major kernel) from lse and delta. */
+int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta,
                       void* stream);
 int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,

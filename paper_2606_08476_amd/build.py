@@ -23,6 +23,7 @@ SOURCES = [
     "host/api.cpp",
     "kernels/attn_fwd.hip",
     "kernels/attn_bwd.hip",
+    "kernels/attn_bwd_dq.hip",
     "kernels/elementwise.hip",
 ]
 

@@ -202,15 +202,15 @@ int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const f
                     "lse_merge launch");
 }
 
-int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta, float* dq,
+int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta,
                       void* stream) {
   fc::clear_error();
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
-  if (!o || !dout || !delta || !dq) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  if (!o || !dout || !delta) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
   return hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o),
-                                               static_cast<const uint16_t*>(dout), delta, dq,
+                                               static_cast<const uint16_t*>(dout), delta,
                                                v->t_q(), v->hq, v->d,
                                                reinterpret_cast<hipStream_t>(stream)),
                     "bwd preprocess launch");
@@ -245,14 +245,33 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
   p.hkv = v->hkv;
   p.group = v->hq / v->hkv;
   p.scale = resolve_scale(scale, v->d);
-  p.dq = dq;
   p.dk_loc = dk_loc;
   p.dv_loc = dv_loc;
   p.dk_recv = dk_recv;
   p.dv_recv = dv_recv;
   p.t_q = v->t_q();
-  return hip_status(fck::launch_bwd(p, v->d, reinterpret_cast<hipStream_t>(stream)),
-                    "attn_bwd launch");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (int rc = hip_status(fck::launch_bwd(p, v->d, s), "attn_bwd dK/dV launch")) return rc;
+  fck::DqParams d{};
+  d.q = p.q;
+  d.dout = p.dout;
+  d.lse = lse;
+  d.delta = delta;
+  d.k_loc = p.k_loc;
+  d.v_loc = p.v_loc;
+  d.k_recv = p.k_recv;
+  d.v_recv = p.v_recv;
+  d.items = m + v->off.fwd_fused;
+  d.perm = m + v->off.perm_fwd_fused;
+  d.n_items = int32_t(v->fwd_fused.size() / 8);
+  d.hq = v->hq;
+  d.hkv = v->hkv;
+  d.group = v->hq / v->hkv;
+  d.head_chunks = d.group / v->heads_per_tile;
+  d.scale = p.scale;
+  d.dq = dq;
+  d.t_q = v->t_q();
+  return hip_status(fck::launch_bwd_dq(d, v->d, v->heads_per_tile, s), "attn_bwd dQ launch");
 }
 
 int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
@@ -273,7 +292,7 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
   if (!q || !k_loc || !v_loc || !lse || !dout || !dq || !dk_loc || !dv_loc ||
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  if (int rc = fc_bwd_preprocess(view, o, dout, delta, dq, stream)) return rc;
+  if (int rc = fc_bwd_preprocess(view, o, dout, delta, stream)) return rc;
   return fc_attn_bwd_pass(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq,
                           dk_loc, dv_loc, dk_recv, dv_recv, stream);
 }

@@ -1,0 +1,188 @@
+// Backward attention, dQ part (gfx950), query-major.
+//
+// Same work items and schedule as the fused forward: one workgroup takes a
+// tile of query tokens of one piece for `heads_per_tile` query heads of one
+// KV head, and walks the received key range (no mask) and then the local key
+// range (intra-document causal). Key/value tiles of 64 keys are
+// double-buffered in LDS and shared by the waves, i.e. by the heads of the
+// group. Per tile, with a query per lane:
+//   S^T = K Q^T, dP^T = V dO^T      Q and dO held in registers;
+//   P = exp(S - LSE), dS = P (dP - D)  LSE and D are per-lane scalars;
+//   dQ^T += K^T dS^T                 K^T read from LDS with transpose reads.
+// dQ is produced whole by the workgroup that owns the query rows, so it is
+// written once, without atomics, and is deterministic. Recomputing S and dP
+// here costs two extra products per key tile compared with accumulating dQ
+// inside the key-major kernel, but removes that kernel's dQ traffic and
+// frees the registers and LDS that limit its occupancy.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace fck {
+
+template <int D, int HPW>
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
+  constexpr int BN = 64;
+  constexpr int WPH = 4 / HPW;
+  constexpr int KS = D / 16;
+  constexpr int DB = D / 32;
+  constexpr int LD = D + 8;
+  constexpr int CH = D / 8;
+  constexpr int PF = BN * CH / 256;
+  __shared__ __attribute__((aligned(16))) u16 sK[2][BN * LD];
+  __shared__ __attribute__((aligned(16))) u16 sV[2][BN * LD];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int b = blockIdx.x;
+  const int kvh = b % p.hkv;
+  const int rest = b / p.hkv;
+  const int hc = rest % p.head_chunks;
+  const int32_t* it = p.items + 8 * p.perm[rest / p.head_chunks];
+  const int q0 = it[0], q1 = it[1], r0 = it[2], r1 = it[3], l0 = it[4], l1 = it[5];
+  const int ldiag = it[6];
+
+  const int h = kvh * p.group + hc * HPW + wave / WPH;
+  const int qrow = q0 + (wave % WPH) * 32 + (lane & 31);
+  const bool qvalid = qrow < q1;
+  const float sl2 = p.scale * kLog2e;
+
+  const int n_r = (r1 - r0 + BN - 1) / BN;
+  const int n_t = n_r + (l1 - l0 + BN - 1) / BN;
+
+  bf16x8 kpf[PF], vpf[PF];
+  auto fetch = [&](int j) {
+    const bool rs = j < n_r;
+    const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
+    const int hi = rs ? r1 : l1;
+    const u16* Kg = rs ? p.k_recv : p.k_loc;
+    const u16* Vg = rs ? p.v_recv : p.v_loc;
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int cidx = threadIdx.x + 256 * u;
+      const int r = cidx / CH, cc = cidx % CH;
+      kpf[u] = zero8();
+      vpf[u] = zero8();
+      if (k0 + r < hi) {
+        const size_t g = ((size_t)(k0 + r) * p.hkv + kvh) * D + cc * 8;
+        kpf[u] = *reinterpret_cast<const bf16x8*>(Kg + g);
+        vpf[u] = *reinterpret_cast<const bf16x8*>(Vg + g);
+      }
+    }
+  };
+  auto commit = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int cidx = threadIdx.x + 256 * u;
+      const int r = cidx / CH, cc = cidx % CH;
+      *reinterpret_cast<bf16x8*>(&sK[buf][r * LD + cc * 8]) = kpf[u];
+      *reinterpret_cast<bf16x8*>(&sV[buf][r * LD + cc * 8]) = vpf[u];
+    }
+  };
+
+  if (n_t > 0) {
+    fetch(0);
+    commit(0);
+  }
+
+  bf16x8 qreg[KS], oreg[KS];
+  float lse2 = 0.f, del = 0.f;
+  {
+    const size_t rb = ((size_t)qrow * p.hq + h) * D + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qreg[ks] = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + rb + 16 * ks) : zero8();
+      oreg[ks] = qvalid ? *reinterpret_cast<const bf16x8*>(p.dout + rb + 16 * ks) : zero8();
+    }
+    if (qvalid) {
+      lse2 = p.lse[(size_t)h * p.t_q + qrow] * kLog2e;
+      del = p.delta[(size_t)h * p.t_q + qrow];
+    }
+  }
+
+  f32x16 dq[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) dq[db] = zero16();
+  __syncthreads();
+
+  for (int j = 0; j < n_t; ++j) {
+    const int buf = j & 1;
+    if (j + 1 < n_t) fetch(j + 1);
+    const bool rs = j < n_r;
+    const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
+    const int hi = rs ? r1 : l1;
+    const u16* K = sK[buf];
+    const u16* V = sV[buf];
+
+    f32x16 s[2], dp[2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      s[mb] = zero16();
+      dp[mb] = zero16();
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int e = (mb * 32 + (lane & 31)) * LD + 16 * ks + 8 * half;
+        s[mb] = mfma32(lds_read8(K, e), qreg[ks], s[mb]);
+        dp[mb] = mfma32(lds_read8(V, e), oreg[ks], dp[mb]);
+      }
+    }
+    const bool diag = !rs && k0 >= ldiag;
+    const bool edge = diag || k0 + BN > hi;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], sl2, -lse2));
+        if (edge) {
+          const int kr = k0 + mb * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
+          const bool vis = kr < hi && (!diag || kr <= qrow);
+          pij = vis ? pij : 0.f;
+        }
+        dp[mb][i] = pij * (dp[mb][i] - del);
+      }
+    // dQ^T += K^T dS^T, 16 keys per MFMA step
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const bf16x8 sb = pack8(dp[kk >> 1], 8 * (kk & 1));
+      const int rb = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * half;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        dq[db] = mfma32(lds_operand_tr(K, LD, rb, rb + 8, 32 * db, lane), sb, dq[db]);
+    }
+    if (j + 1 < n_t) commit(buf ^ 1);
+    __syncthreads();
+  }
+
+  if (qvalid) {
+    float* out = p.dq + ((size_t)qrow * p.hq + h) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4 v;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) v[jj] = p.scale * dq[db][4 * g + jj];
+        *reinterpret_cast<f32x4*>(out + 32 * db + 8 * g + 4 * half) = v;
+      }
+  }
+}
+
+template <int D>
+static hipError_t launch_dq_d(const DqParams& p, int hpw, hipStream_t s) {
+  const dim3 grid(unsigned(p.n_items) * p.hkv * p.head_chunks), block(256);
+  switch (hpw) {
+    case 1: hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 1>), grid, block, 0, s, p); break;
+    case 2: hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 2>), grid, block, 0, s, p); break;
+    case 4: hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 4>), grid, block, 0, s, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq(const DqParams& p, int d, int heads_per_tile, hipStream_t s) {
+  if (p.n_items == 0) return hipSuccess;
+  if (d == 64) return launch_dq_d<64>(p, heads_per_tile, s);
+  if (d == 128) return launch_dq_d<128>(p, heads_per_tile, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace fck

@@ -4,13 +4,16 @@
 // with a received key range (no mask inside it, FlashCP Sec. 3.2: every
 // query of a piece sees the same received prefix) and a local key range
 // (intra-document causal, Sec. 2.1) -- for `heads_per_tile` query heads of
-// one KV head. Each wave owns 32 query rows of one head. Per key tile of 64
-// keys, staged in LDS and shared by the waves (and so by the heads of the
-// group):
+// one KV head. Each wave owns 32 query rows of one head. Key tiles of 64
+// keys are double-buffered in LDS and shared by the waves (and so by the
+// heads of the group); the next tile's global loads are in flight while the
+// current one is computed:
 //   S^T = K Q^T        MFMA 32x32x16, Q held in registers (B operand), so a
 //                      query is a lane and its row statistics are per lane;
-//   online softmax     base-2, running max/sum per lane, one cross-half
-//                      exchange per tile;
+//   online softmax     base 2, scale folded into one FMA per score; the
+//                      output is rescaled only when a row maximum grows by
+//                      more than 2^8 (the result is the same: numerator and
+//                      denominator share the stale maximum);
 //   O^T += V^T P^T     V^T read from LDS with transpose reads, P^T straight
 //                      from the S^T accumulator registers.
 // Output: the final O (bf16, optionally fp32) and LSE, or an fp32 partial
@@ -21,15 +24,17 @@
 namespace fck {
 
 template <int D, int HPW, bool FINAL>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams p) {
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   constexpr int BN = 64;        // keys per tile
   constexpr int WPH = 4 / HPW;  // waves per query head
   constexpr int KS = D / 16;    // MFMA k-steps over the head dim
   constexpr int DB = D / 32;    // 32-wide output blocks of the head dim
   constexpr int LD = D + 8;     // padded LDS row (elements)
   constexpr int CH = D / 8;     // 16-byte chunks per row
-  __shared__ __attribute__((aligned(16))) u16 sK[BN * LD];
-  __shared__ __attribute__((aligned(16))) u16 sV[BN * LD];
+  constexpr int PF = BN * CH / 256;  // chunks per thread per tensor
+  constexpr float kLazy = 8.0f;      // log2 headroom before rescaling
+  __shared__ __attribute__((aligned(16))) u16 sK[2][BN * LD];
+  __shared__ __attribute__((aligned(16))) u16 sV[2][BN * LD];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5;
@@ -44,6 +49,46 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams p) {
   const int h = kvh * p.group + hc * HPW + wave / WPH;
   const int qrow = q0 + (wave % WPH) * 32 + (lane & 31);
   const bool qvalid = qrow < q1;
+  const float c = p.scale_log2;
+
+  // key tiles: first the received range, then the local range
+  const int n_r = (r1 - r0 + BN - 1) / BN;
+  const int n_t = n_r + (l1 - l0 + BN - 1) / BN;
+
+  bf16x8 kpf[PF], vpf[PF];
+  auto fetch = [&](int j) {
+    const bool rs = j < n_r;
+    const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
+    const int hi = rs ? r1 : l1;
+    const u16* Kg = rs ? p.k_recv : p.k_loc;
+    const u16* Vg = rs ? p.v_recv : p.v_loc;
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int cidx = threadIdx.x + 256 * u;
+      const int r = cidx / CH, cc = cidx % CH;
+      kpf[u] = zero8();
+      vpf[u] = zero8();
+      if (k0 + r < hi) {
+        const size_t g = ((size_t)(k0 + r) * p.hkv + kvh) * D + cc * 8;
+        kpf[u] = *reinterpret_cast<const bf16x8*>(Kg + g);
+        vpf[u] = *reinterpret_cast<const bf16x8*>(Vg + g);
+      }
+    }
+  };
+  auto commit = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int cidx = threadIdx.x + 256 * u;
+      const int r = cidx / CH, cc = cidx % CH;
+      *reinterpret_cast<bf16x8*>(&sK[buf][r * LD + cc * 8]) = kpf[u];
+      *reinterpret_cast<bf16x8*>(&sV[buf][r * LD + cc * 8]) = vpf[u];
+    }
+  };
+
+  if (n_t > 0) {
+    fetch(0);
+    commit(0);
+  }
 
   bf16x8 qreg[KS];
   {
@@ -56,92 +101,84 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams p) {
   f32x16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) oacc[db] = zero16();
-  float m = -INFINITY;  // running row max (log2 units)
+  float m = -INFINITY;  // reference row maximum (scaled, log2 units)
   float lsum = 0.f;     // this lane's share of the row sum
+  __syncthreads();
 
-  for (int src = 0; src < 2; ++src) {
-    const int lo = src == 0 ? r0 : l0;
-    const int hi = src == 0 ? r1 : l1;
-    const u16* Kg = src == 0 ? p.k_recv : p.k_loc;
-    const u16* Vg = src == 0 ? p.v_recv : p.v_loc;
-    for (int k0 = lo; k0 < hi; k0 += BN) {
-      __syncthreads();  // the previous tile is consumed
-      for (int c = threadIdx.x; c < BN * CH; c += 256) {
-        const int r = c / CH, cc = c % CH;
-        bf16x8 kv = zero8(), vv = zero8();
-        if (k0 + r < hi) {
-          const size_t g = ((size_t)(k0 + r) * p.hkv + kvh) * D + cc * 8;
-          kv = *reinterpret_cast<const bf16x8*>(Kg + g);
-          vv = *reinterpret_cast<const bf16x8*>(Vg + g);
-        }
-        *reinterpret_cast<bf16x8*>(sK + r * LD + cc * 8) = kv;
-        *reinterpret_cast<bf16x8*>(sV + r * LD + cc * 8) = vv;
-      }
-      __syncthreads();
+  for (int j = 0; j < n_t; ++j) {
+    const int buf = j & 1;
+    if (j + 1 < n_t) fetch(j + 1);
+    const bool rs = j < n_r;
+    const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
+    const int hi = rs ? r1 : l1;
+    const u16* K = sK[buf];
+    const u16* V = sV[buf];
 
-      f32x16 s[2];
+    f32x16 s[2];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        s[mb] = zero16();
+    for (int mb = 0; mb < 2; ++mb) {
+      s[mb] = zero16();
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          s[mb] = mfma32(lds_read8(sK, (mb * 32 + (lane & 31)) * LD + 16 * ks + 8 * half),
-                         qreg[ks], s[mb]);
-      }
-      // scale; mask keys past the range and, on diagonal tiles, later keys
-      const bool diag = src == 1 && k0 >= ldiag;
-      const bool edge = diag || k0 + BN > hi;
-      float mx = -INFINITY;
+      for (int ks = 0; ks < KS; ++ks)
+        s[mb] = mfma32(lds_read8(K, (mb * 32 + (lane & 31)) * LD + 16 * ks + 8 * half), qreg[ks],
+                       s[mb]);
+    }
+    // mask keys past the range and, on diagonal tiles, keys after the query
+    const bool diag = !rs && k0 >= ldiag;
+    if (diag || k0 + BN > hi) {
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
+      for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          float x = s[mb][i] * p.scale_log2;
-          if (edge) {
-            const int kr = k0 + mb * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
-            const bool vis = kr < hi && (!diag || kr <= qrow);
-            x = vis ? x : -INFINITY;
-          }
-          s[mb][i] = x;
-          mx = fmaxf(mx, x);
+          const int kr = k0 + mb * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
+          const bool vis = kr < hi && (!diag || kr <= qrow);
+          s[mb][i] = vis ? s[mb][i] : -INFINITY;
         }
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[mb][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
+    if (__any(mx > m + kLazy)) {
       const float mnew = fmaxf(m, mx);
-      const float mref = mnew == -INFINITY ? 0.f : mnew;
-      const float alpha = exp2f(m - mref);
+      const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mnew);
       m = mnew;
-      float ps = 0.f;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float e = exp2f(s[mb][i] - mref);
-          s[mb][i] = e;
-          ps += e;
-        }
-      }
-      lsum = lsum * alpha + ps;
+      lsum *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-
-      // O^T += V^T P^T, 16 keys per MFMA step
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 pb = pack8(s[kk >> 1], 8 * (kk & 1));
-        const int rb = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * half;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-          oacc[db] = mfma32(lds_operand_tr(sV, LD, rb, rb + 8, 32 * db, lane), pb, oacc[db]);
-      }
     }
+    const float mref = m == -INFINITY ? 0.f : m;
+    float ps = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], c, -mref));
+        s[mb][i] = e;
+        ps += e;
+      }
+    lsum += ps;
+
+    // O^T += V^T P^T, 16 keys per MFMA step
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const bf16x8 pb = pack8(s[kk >> 1], 8 * (kk & 1));
+      const int rb = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * half;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        oacc[db] = mfma32(lds_operand_tr(V, LD, rb, rb + 8, 32 * db, lane), pb, oacc[db]);
+    }
+    if (j + 1 < n_t) commit(buf ^ 1);
+    __syncthreads();
   }
 
   lsum += __shfl_xor(lsum, 32);
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-  const float lse = lsum > 0.f ? (m + log2f(lsum)) * kLn2 : -INFINITY;
+  const float lse = lsum > 0.f ? (m + __log2f(lsum)) * kLn2 : -INFINITY;
   if (qvalid) {
     const size_t ob = ((size_t)qrow * p.hq + h) * D;
 #pragma unroll
@@ -151,7 +188,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams p) {
         const int dcol = 32 * db + 8 * g + 4 * half;
         f32x4 v;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = oacc[db][4 * g + j] * inv;
+        for (int jj = 0; jj < 4; ++jj) v[jj] = oacc[db][4 * g + jj] * inv;
         if (FINAL) {
           uint2 packed;
           packed.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);

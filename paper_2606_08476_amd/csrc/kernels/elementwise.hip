@@ -62,13 +62,11 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const float* __restrict_
   if (c == 0) lse_out[li] = m + __logf(tot);
 }
 
-// delta[head, tok] = sum_d dO * O over one (token, head) row; also zeroes
-// the row of dq, which the backward accumulates into.
+// delta[head, tok] = sum_d dO * O over one (token, head) row.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(const u16* __restrict__ o,
                                                       const u16* __restrict__ dout,
-                                                      float* delta, float* dq, int32_t t,
-                                                      int32_t h) {
+                                                      float* delta, int32_t t, int32_t h) {
   constexpr int LPR = D / 8;  // lanes per row, 8 values each
   const int64_t row = (int64_t(blockIdx.x) * 256 + threadIdx.x) / LPR;
   const int c = threadIdx.x % LPR;
@@ -83,9 +81,6 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const u16* __restrict__ o,
       acc += bf2f(u16(aw[j] & 0xffff)) * bf2f(u16(gw[j] & 0xffff));
       acc += bf2f(u16(aw[j] >> 16)) * bf2f(u16(gw[j] >> 16));
     }
-    f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    reinterpret_cast<f32x4*>(dq + row * D)[2 * c] = z;
-    reinterpret_cast<f32x4*>(dq + row * D)[2 * c + 1] = z;
   }
 #pragma unroll
   for (int w = LPR / 2; w >= 1; w >>= 1) acc += __shfl_xor(acc, w);
@@ -133,16 +128,16 @@ hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta, float* dq,
+hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta,
                                  int32_t t, int32_t h, int32_t d, hipStream_t s) {
   const int64_t rows = int64_t(t) * h;
   if (rows == 0) return hipSuccess;
   if (d == 64)
     hipLaunchKernelGGL(bwd_pre_kernel<64>, dim3(grid_for(rows * 8)), dim3(256), 0, s, o, dout,
-                       delta, dq, t, h);
+                       delta, t, h);
   else if (d == 128)
     hipLaunchKernelGGL(bwd_pre_kernel<128>, dim3(grid_for(rows * 16)), dim3(256), 0, s, o, dout,
-                       delta, dq, t, h);
+                       delta, t, h);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

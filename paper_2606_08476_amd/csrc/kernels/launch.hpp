@@ -40,7 +40,6 @@ struct BwdParams {
   int32_t n_items;
   int32_t hq, hkv, group;
   float scale;
-  float* dq;                // [t_q, hq, d] fp32, accumulated atomically
   float* dk_loc;            // [t_q, hkv, d] fp32
   float* dv_loc;
   float* dk_recv;           // [t_r, hkv, d] fp32
@@ -48,10 +47,29 @@ struct BwdParams {
   int32_t t_q;
 };
 
+struct DqParams {
+  const uint16_t* q;        // [t_q, hq, d]
+  const uint16_t* dout;     // [t_q, hq, d]
+  const float* lse;         // [hq, t_q] natural log
+  const float* delta;       // [hq, t_q]
+  const uint16_t* k_recv;
+  const uint16_t* v_recv;
+  const uint16_t* k_loc;
+  const uint16_t* v_loc;
+  const int32_t* items;     // fused forward items: q0 q1 r0 r1 l0 l1 ldiag seg
+  const int32_t* perm;
+  int32_t n_items;
+  int32_t hq, hkv, group, head_chunks;
+  float scale;
+  float* dq;                // [t_q, hq, d] fp32, written
+  int32_t t_q;
+};
+
 hipError_t launch_fwd(const FwdParams& p, int d, int heads_per_tile, bool final_out,
                       hipStream_t s);
+hipError_t launch_bwd_dq(const DqParams& p, int d, int heads_per_tile, hipStream_t s);
 hipError_t launch_bwd(const BwdParams& p, int d, hipStream_t s);
-hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta, float* dq,
+hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta,
                                  int32_t t, int32_t h, int32_t d, hipStream_t s);
 hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o_b,
                             const float* lse_b, int32_t t, int32_t h, int32_t d, uint16_t* o_bf16,

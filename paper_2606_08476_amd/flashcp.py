@@ -91,7 +91,7 @@ def lib():
             "fc_attn_fwd_partial": [P, C.c_int32, P, P, P, C.c_float, P, P, P],
             "fc_lse_merge": [P, P, P, P, C.c_int32, C.c_int32, C.c_int32, P, P, P, P],
             "fc_attn_bwd": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P, C.c_size_t, P],
-            "fc_bwd_preprocess": [P, P, P, P, P, P],
+            "fc_bwd_preprocess": [P, P, P, P, P],
             "fc_attn_bwd_pass": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P],
         }
         for name, args in sig.items():
@@ -341,13 +341,13 @@ def fc_attn_bwd(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale
         _stream()))
 
 
-def fc_bwd_preprocess(view: View, o, dout, delta, dq):
+def fc_bwd_preprocess(view: View, o, dout, delta):
     import torch
     i = view.info
     tq, hq, d = i["t_q"], i["hq"], i["d"]
     _check(lib().fc_bwd_preprocess(
         view.handle, _ptr(o, (tq, hq, d), torch.bfloat16, "o"), _ptr(dout, (tq, hq, d), torch.bfloat16, "dout"),
-        _ptr(delta, (hq, tq), torch.float32, "delta"), _ptr(dq, (tq, hq, d), torch.float32, "dq"), _stream()))
+        _ptr(delta, (hq, tq), torch.float32, "delta"), _stream()))
 
 
 def fc_attn_bwd_pass(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
