@@ -150,7 +150,8 @@ def main():
     dk_recv = torch.empty(tr, hkv, d, dtype=f32, device=dev)
     dv_recv = torch.empty_like(dk_recv)
     meta = torch.empty(int(info["meta_bytes"]) + 256, dtype=torch.uint8, device=dev)
-    names = ["kv_gather", "attn_fwd_local", "attn_fwd_recv", "lse_merge", "bwd_preprocess", "attn_bwd"]
+    names = ["kv_gather", "attn_fwd_local", "attn_fwd_recv", "lse_merge", "bwd_preprocess",
+             "attn_bwd_dkdv", "attn_bwd_dq"]
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
     acc = np.zeros(len(names))
     kept = []
@@ -173,9 +174,11 @@ def main():
         ev[4].record()
         F.fc_bwd_preprocess(v, o, do, delta)
         ev[5].record()
-        F.fc_attn_bwd_pass(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq, dk_loc,
+        F.fc_attn_bwd_dkdv(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dk_loc,
                            dv_loc, dk_recv, dv_recv)
         ev[6].record()
+        F.fc_attn_bwd_dq(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq)
+        ev[7].record()
 
     for _ in range(args.warmup):
         step(False)
@@ -209,7 +212,9 @@ def main():
         "attn_fwd_recv": ("mfma", 4.0 * d * hq * info["pairs_recv"]),
         "lse_merge": ("hbm", tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4)),
         "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4)),
-        "attn_bwd": ("mfma", 10.0 * d * hq * pairs),
+        # dK/dV pass: S, dP, dV, dK (8d per pair); dQ pass: S, dP again and dQ (6d)
+        "attn_bwd_dkdv": ("mfma", 8.0 * d * hq * pairs),
+        "attn_bwd_dq": ("mfma", 6.0 * d * hq * pairs),
     }
     kernels = {}
     for i, n in enumerate(names):

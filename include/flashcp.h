@@ -226,6 +226,15 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
  * kernel) and dq (query-major kernel) from lse and delta. */
 int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta,
                       void* stream);
+/* The two kernels of fc_attn_bwd_pass, callable alone: the key-major
+ * dK/dV pass (writes dk_*, dv_*) and the query-major dQ pass (writes dq). */
+int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                     const void* k_recv, const void* v_recv, const float* lse, const float* delta,
+                     const void* dout, float scale, float* dk_loc, float* dv_loc, float* dk_recv,
+                     float* dv_recv, void* stream);
+int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                   const void* k_recv, const void* v_recv, const float* lse, const float* delta,
+                   const void* dout, float scale, float* dq, void* stream);
 int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,
                      const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,

@@ -216,15 +216,15 @@ int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delt
                     "bwd preprocess launch");
 }
 
-int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,
-                     const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                     float* dk_recv, float* dv_recv, void* stream) {
+                     const void* dout, float scale, float* dk_loc, float* dv_loc, float* dk_recv,
+                     float* dv_recv, void* stream) {
   fc::clear_error();
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
-  if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dq || !dk_loc || !dv_loc ||
+  if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dk_loc || !dv_loc ||
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
   const int32_t* m = v->dev_meta;
@@ -250,17 +250,30 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
   p.dk_recv = dk_recv;
   p.dv_recv = dv_recv;
   p.t_q = v->t_q();
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (int rc = hip_status(fck::launch_bwd(p, v->d, s), "attn_bwd dK/dV launch")) return rc;
+  return hip_status(fck::launch_bwd(p, v->d, reinterpret_cast<hipStream_t>(stream)),
+                    "attn_bwd dK/dV launch");
+}
+
+int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                   const void* k_recv, const void* v_recv, const float* lse, const float* delta,
+                   const void* dout, float scale, float* dq, void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (v->t_q() == 0) return FC_OK;
+  if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dq ||
+      (v->t_recv() && (!k_recv || !v_recv)))
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  const int32_t* m = v->dev_meta;
   fck::DqParams d{};
-  d.q = p.q;
-  d.dout = p.dout;
+  d.q = static_cast<const uint16_t*>(q);
+  d.dout = static_cast<const uint16_t*>(dout);
   d.lse = lse;
   d.delta = delta;
-  d.k_loc = p.k_loc;
-  d.v_loc = p.v_loc;
-  d.k_recv = p.k_recv;
-  d.v_recv = p.v_recv;
+  d.k_loc = static_cast<const uint16_t*>(k_loc);
+  d.v_loc = static_cast<const uint16_t*>(v_loc);
+  d.k_recv = static_cast<const uint16_t*>(k_recv);
+  d.v_recv = static_cast<const uint16_t*>(v_recv);
   d.items = m + v->off.fwd_fused;
   d.perm = m + v->off.perm_fwd_fused;
   d.n_items = int32_t(v->fwd_fused.size() / 8);
@@ -268,10 +281,28 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
   d.hkv = v->hkv;
   d.group = v->hq / v->hkv;
   d.head_chunks = d.group / v->heads_per_tile;
-  d.scale = p.scale;
+  d.scale = resolve_scale(scale, v->d);
   d.dq = dq;
   d.t_q = v->t_q();
-  return hip_status(fck::launch_bwd_dq(d, v->d, v->heads_per_tile, s), "attn_bwd dQ launch");
+  return hip_status(fck::launch_bwd_dq(d, v->d, v->heads_per_tile,
+                                       reinterpret_cast<hipStream_t>(stream)),
+                    "attn_bwd dQ launch");
+}
+
+int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                     const void* k_recv, const void* v_recv, const float* lse, const float* delta,
+                     const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
+                     float* dk_recv, float* dv_recv, void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (v->t_q() == 0) return FC_OK;
+  if (!dq) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  if (int rc = fc_attn_bwd_dkdv(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
+                                dk_loc, dv_loc, dk_recv, dv_recv, stream))
+    return rc;
+  return fc_attn_bwd_dq(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq,
+                        stream);
 }
 
 int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,

@@ -5,9 +5,9 @@
 // the tile accumulate in registers, summed over every query head of the
 // group (grouped-query attention) and every query tile that sees the keys.
 // K sits in LDS, V in registers. The (query head, 32-query tile) iterations
-// are software-pipelined: the next tile's Q, dO, LSE and D are loaded from
-// HBM while the current one is computed, into a second LDS buffer. Per
-// iteration:
+// are software-pipelined: the next tile's Q and dO are copied from HBM
+// straight into a second LDS buffer (asynchronous loads) while the current
+// one is computed. Per iteration:
 //   S  = Q K^T, dP = dO V^T     MFMA (Q, dO, K from LDS, V from registers);
 //   P  = exp(S - LSE), dS = P (dP - D)   D = rowsum(dO * O) from the
 //                               preprocess kernel, LSE the merged forward LSE;
@@ -27,14 +27,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   constexpr int BM = 32;        // queries per iteration
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
-  constexpr int LD = D + 8;
-  constexpr int CH = D / 8;
-  constexpr int PF = BM * CH / 256;         // 16-byte chunks per thread per tensor
-  __shared__ __attribute__((aligned(16))) u16 sK[BN * LD];
-  __shared__ __attribute__((aligned(16))) u16 sQ[2][BM * LD];
-  __shared__ __attribute__((aligned(16))) u16 sO[2][BM * LD];  // dO tiles
-  __shared__ __attribute__((aligned(16))) float sL[2][BM];     // LSE * log2(e)
-  __shared__ __attribute__((aligned(16))) float sD[2][BM];     // delta
+  __shared__ __attribute__((aligned(16))) u16 sK[BN * D];
+  __shared__ __attribute__((aligned(16))) u16 sQ[2][BM * D];
+  __shared__ __attribute__((aligned(16))) u16 sO[2][BM * D];  // dO tiles
+  __shared__ __attribute__((aligned(16))) float sL[2][BM];    // LSE
+  __shared__ __attribute__((aligned(16))) float sD[2][BM];    // delta
   __shared__ __attribute__((aligned(16))) int sLim[2][BM];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -47,20 +44,17 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   const u16* Vg = src ? p.v_recv : p.v_loc;
   float* dKg = src ? p.dk_recv : p.dk_loc;
   float* dVg = src ? p.dv_recv : p.dv_loc;
+  const size_t kvs = size_t(p.hkv) * D, kvo = size_t(kvh) * D;
 
-  for (int c = threadIdx.x; c < BN * CH; c += 256) {
-    const int r = c / CH, cc = c % CH;
-    bf16x8 kv = zero8();
-    if (k0 + r < k1) kv = *reinterpret_cast<const bf16x8*>(Kg + ((size_t)(k0 + r) * p.hkv + kvh) * D + cc * 8);
-    *reinterpret_cast<bf16x8*>(sK + r * LD + cc * 8) = kv;
-  }
+  // key tile (rows past k1 repeat the last key; they are masked)
+  tile_load_async<D, BN>(sK, [&](int r) { return Kg + size_t(min(k0 + r, k1 - 1)) * kvs + kvo; });
   const int krow = 32 * wave + (lane & 31);  // this lane's key within the tile
   const int kidx = k0 + krow;
   const bool kvalid = kidx < k1;
   // V rows of this lane's key as the B operand of dP = dO V^T
   bf16x8 vreg[KS];
   {
-    const u16* vp = Vg + ((size_t)kidx * p.hkv + kvh) * D + 8 * half;
+    const u16* vp = Vg + size_t(kidx) * kvs + kvo + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       vreg[ks] = kvalid ? *reinterpret_cast<const bf16x8*>(vp + 16 * ks) : zero8();
@@ -69,40 +63,23 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   const int ntile = (q1 - q0 + BM - 1) / BM;
   const int n_it = ntile * p.group;
 
-  bf16x8 qpf[PF], opf[PF];
+  // next iteration: Q/dO tiles straight into LDS, LSE/D/limit via registers
   float lpf = 0.f, dpf = 0.f;
   int mpf = 0;
-  auto fetch = [&](int i_) {
+  auto fetch = [&](int i_, int buf) {
     const int h = kvh * p.group + i_ / ntile;
     const int t0 = q0 + (i_ % ntile) * BM;
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int cidx = threadIdx.x + 256 * u;
-      const int r = cidx / CH, cc = cidx % CH;
-      qpf[u] = zero8();
-      opf[u] = zero8();
-      if (t0 + r < q1) {
-        const size_t g = ((size_t)(t0 + r) * p.hq + h) * D + cc * 8;
-        qpf[u] = *reinterpret_cast<const bf16x8*>(p.q + g);
-        opf[u] = *reinterpret_cast<const bf16x8*>(p.dout + g);
-      }
-    }
+    const size_t qs = size_t(p.hq) * D, qo = size_t(h) * D;
+    tile_load_async<D, BM>(sQ[buf], [&](int r) { return p.q + size_t(min(t0 + r, q1 - 1)) * qs + qo; });
+    tile_load_async<D, BM>(sO[buf], [&](int r) { return p.dout + size_t(min(t0 + r, q1 - 1)) * qs + qo; });
     if (threadIdx.x < BM) {
-      const int qi = t0 + threadIdx.x;
-      const bool ok = qi < q1;
-      lpf = ok ? p.lse[(size_t)h * p.t_q + qi] * kLog2e : 0.f;
-      dpf = ok ? p.delta[(size_t)h * p.t_q + qi] : 0.f;
-      mpf = ok ? p.lim[qi] : 0;
+      const int qi = min(t0 + int(threadIdx.x), q1 - 1);
+      lpf = p.lse[(size_t)h * p.t_q + qi];
+      dpf = p.delta[(size_t)h * p.t_q + qi];
+      mpf = p.lim[qi];
     }
   };
   auto commit = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int cidx = threadIdx.x + 256 * u;
-      const int r = cidx / CH, cc = cidx % CH;
-      *reinterpret_cast<bf16x8*>(&sQ[buf][r * LD + cc * 8]) = qpf[u];
-      *reinterpret_cast<bf16x8*>(&sO[buf][r * LD + cc * 8]) = opf[u];
-    }
     if (threadIdx.x < BM) {
       sL[buf][threadIdx.x] = lpf;
       sD[buf][threadIdx.x] = dpf;
@@ -120,24 +97,26 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   const float sl2 = p.scale * kLog2e;
 
   if (n_it > 0) {
-    fetch(0);
+    fetch(0, 0);
+    wait_async();
     commit(0);
   }
+  wait_async();
   __syncthreads();
 
   for (int i_ = 0; i_ < n_it; ++i_) {
     const int buf = i_ & 1;
     const int t0 = q0 + (i_ % ntile) * BM;
-    if (i_ + 1 < n_it) fetch(i_ + 1);
+    if (i_ + 1 < n_it) fetch(i_ + 1, buf ^ 1);
     const u16* Q = sQ[buf];
     const u16* O = sO[buf];
 
     f32x16 sacc = zero16(), dpacc = zero16();
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const int eq = (lane & 31) * LD + 16 * ks + 8 * half;
-      sacc = mfma32(lds_read8(Q, eq), lds_read8(sK, krow * LD + 16 * ks + 8 * half), sacc);
-      dpacc = mfma32(lds_read8(O, eq), vreg[ks], dpacc);
+      const int col = 16 * ks + 8 * half;
+      sacc = mfma32(tread8<D>(Q, lane & 31, col), tread8<D>(sK, krow, col), sacc);
+      dpacc = mfma32(tread8<D>(O, lane & 31, col), vreg[ks], dpacc);
     }
     // this lane's 16 query rows are 8g + 4*half + 0..3, g = 0..3
     const bool diag = t0 < qfull;
@@ -152,7 +131,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int i = 4 * g + j;
-        float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -l4[j]));
+        float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -l4[j] * kLog2e));
         if (edge) {
           const int qi = t0 + 8 * g + 4 * half + j;
           bool vis = kvalid && qi < q1;
@@ -171,10 +150,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
       const int rb = 16 * kh + 4 * half;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        dv[db] = mfma32(pa, lds_operand_tr(O, LD, rb, rb + 8, 32 * db, lane), dv[db]);
-        dk[db] = mfma32(sa, lds_operand_tr(Q, LD, rb, rb + 8, 32 * db, lane), dk[db]);
+        dv[db] = mfma32(pa, tread_tr<D>(O, rb, rb + 8, 32 * db, lane), dv[db]);
+        dk[db] = mfma32(sa, tread_tr<D>(Q, rb, rb + 8, 32 * db, lane), dk[db]);
       }
     }
+    wait_async();
     if (i_ + 1 < n_it) commit(buf ^ 1);
     __syncthreads();
   }

@@ -4,8 +4,8 @@
 // tile of query tokens of one piece for `heads_per_tile` query heads of one
 // KV head, and walks the received key range (no mask) and then the local key
 // range (intra-document causal). Key/value tiles of 64 keys are
-// double-buffered in LDS and shared by the waves, i.e. by the heads of the
-// group. Per tile, with a query per lane:
+// double-buffered in LDS (asynchronous HBM-to-LDS copies) and shared by the
+// waves, i.e. by the heads of the group. Per tile, with a query per lane:
 //   S^T = K Q^T, dP^T = V dO^T      Q and dO held in registers;
 //   P = exp(S - LSE), dS = P (dP - D)  LSE and D are per-lane scalars;
 //   dQ^T += K^T dS^T                 K^T read from LDS with transpose reads.
@@ -25,11 +25,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
   constexpr int WPH = 4 / HPW;
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
-  constexpr int LD = D + 8;
-  constexpr int CH = D / 8;
-  constexpr int PF = BN * CH / 256;
-  __shared__ __attribute__((aligned(16))) u16 sK[2][BN * LD];
-  __shared__ __attribute__((aligned(16))) u16 sV[2][BN * LD];
+  __shared__ __attribute__((aligned(16))) u16 sK[2][BN * D];
+  __shared__ __attribute__((aligned(16))) u16 sV[2][BN * D];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5;
@@ -49,40 +46,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
   const int n_r = (r1 - r0 + BN - 1) / BN;
   const int n_t = n_r + (l1 - l0 + BN - 1) / BN;
 
-  bf16x8 kpf[PF], vpf[PF];
-  auto fetch = [&](int j) {
+  auto fetch = [&](int j, int buf) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
-    const int hi = rs ? r1 : l1;
+    const int last = (rs ? r1 : l1) - 1;
     const u16* Kg = rs ? p.k_recv : p.k_loc;
     const u16* Vg = rs ? p.v_recv : p.v_loc;
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int cidx = threadIdx.x + 256 * u;
-      const int r = cidx / CH, cc = cidx % CH;
-      kpf[u] = zero8();
-      vpf[u] = zero8();
-      if (k0 + r < hi) {
-        const size_t g = ((size_t)(k0 + r) * p.hkv + kvh) * D + cc * 8;
-        kpf[u] = *reinterpret_cast<const bf16x8*>(Kg + g);
-        vpf[u] = *reinterpret_cast<const bf16x8*>(Vg + g);
-      }
-    }
-  };
-  auto commit = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int cidx = threadIdx.x + 256 * u;
-      const int r = cidx / CH, cc = cidx % CH;
-      *reinterpret_cast<bf16x8*>(&sK[buf][r * LD + cc * 8]) = kpf[u];
-      *reinterpret_cast<bf16x8*>(&sV[buf][r * LD + cc * 8]) = vpf[u];
-    }
+    const size_t hs = size_t(p.hkv) * D, ho = size_t(kvh) * D;
+    tile_load_async<D, BN>(sK[buf], [&](int r) { return Kg + size_t(min(k0 + r, last)) * hs + ho; });
+    tile_load_async<D, BN>(sV[buf], [&](int r) { return Vg + size_t(min(k0 + r, last)) * hs + ho; });
   };
 
-  if (n_t > 0) {
-    fetch(0);
-    commit(0);
-  }
+  if (n_t > 0) fetch(0, 0);
 
   bf16x8 qreg[KS], oreg[KS];
   float lse2 = 0.f, del = 0.f;
@@ -102,11 +77,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
   f32x16 dq[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
+  wait_async();
   __syncthreads();
 
   for (int j = 0; j < n_t; ++j) {
     const int buf = j & 1;
-    if (j + 1 < n_t) fetch(j + 1);
+    if (j + 1 < n_t) fetch(j + 1, buf ^ 1);
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
@@ -120,9 +96,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
       dp[mb] = zero16();
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const int e = (mb * 32 + (lane & 31)) * LD + 16 * ks + 8 * half;
-        s[mb] = mfma32(lds_read8(K, e), qreg[ks], s[mb]);
-        dp[mb] = mfma32(lds_read8(V, e), oreg[ks], dp[mb]);
+        const int row = mb * 32 + (lane & 31), col = 16 * ks + 8 * half;
+        s[mb] = mfma32(tread8<D>(K, row, col), qreg[ks], s[mb]);
+        dp[mb] = mfma32(tread8<D>(V, row, col), oreg[ks], dp[mb]);
       }
     }
     const bool diag = !rs && k0 >= ldiag;
@@ -146,9 +122,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
       const int rb = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * half;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
-        dq[db] = mfma32(lds_operand_tr(K, LD, rb, rb + 8, 32 * db, lane), sb, dq[db]);
+        dq[db] = mfma32(tread_tr<D>(K, rb, rb + 8, 32 * db, lane), sb, dq[db]);
     }
-    if (j + 1 < n_t) commit(buf ^ 1);
+    wait_async();
     __syncthreads();
   }
 

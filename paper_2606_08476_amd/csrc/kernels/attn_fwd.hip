@@ -6,8 +6,9 @@
 // (intra-document causal, Sec. 2.1) -- for `heads_per_tile` query heads of
 // one KV head. Each wave owns 32 query rows of one head. Key tiles of 64
 // keys are double-buffered in LDS and shared by the waves (and so by the
-// heads of the group); the next tile's global loads are in flight while the
-// current one is computed:
+// heads of the group); the next tile is copied from HBM straight into LDS
+// (asynchronous loads, no staging registers) while the current one is
+// computed:
 //   S^T = K Q^T        MFMA 32x32x16, Q held in registers (B operand), so a
 //                      query is a lane and its row statistics are per lane;
 //   online softmax     base 2, scale folded into one FMA per score; the
@@ -29,12 +30,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   constexpr int WPH = 4 / HPW;  // waves per query head
   constexpr int KS = D / 16;    // MFMA k-steps over the head dim
   constexpr int DB = D / 32;    // 32-wide output blocks of the head dim
-  constexpr int LD = D + 8;     // padded LDS row (elements)
-  constexpr int CH = D / 8;     // 16-byte chunks per row
-  constexpr int PF = BN * CH / 256;  // chunks per thread per tensor
-  constexpr float kLazy = 8.0f;      // log2 headroom before rescaling
-  __shared__ __attribute__((aligned(16))) u16 sK[2][BN * LD];
-  __shared__ __attribute__((aligned(16))) u16 sV[2][BN * LD];
+  constexpr float kLazy = 8.0f; // log2 headroom before rescaling
+  __shared__ __attribute__((aligned(16))) u16 sK[2][BN * D];
+  __shared__ __attribute__((aligned(16))) u16 sV[2][BN * D];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5;
@@ -55,40 +53,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int n_r = (r1 - r0 + BN - 1) / BN;
   const int n_t = n_r + (l1 - l0 + BN - 1) / BN;
 
-  bf16x8 kpf[PF], vpf[PF];
-  auto fetch = [&](int j) {
+  // async load of key tile j into buffer `buf`; rows past the range repeat
+  // the last row (finite data; those keys are masked)
+  auto fetch = [&](int j, int buf) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
-    const int hi = rs ? r1 : l1;
+    const int last = (rs ? r1 : l1) - 1;
     const u16* Kg = rs ? p.k_recv : p.k_loc;
     const u16* Vg = rs ? p.v_recv : p.v_loc;
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int cidx = threadIdx.x + 256 * u;
-      const int r = cidx / CH, cc = cidx % CH;
-      kpf[u] = zero8();
-      vpf[u] = zero8();
-      if (k0 + r < hi) {
-        const size_t g = ((size_t)(k0 + r) * p.hkv + kvh) * D + cc * 8;
-        kpf[u] = *reinterpret_cast<const bf16x8*>(Kg + g);
-        vpf[u] = *reinterpret_cast<const bf16x8*>(Vg + g);
-      }
-    }
-  };
-  auto commit = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int cidx = threadIdx.x + 256 * u;
-      const int r = cidx / CH, cc = cidx % CH;
-      *reinterpret_cast<bf16x8*>(&sK[buf][r * LD + cc * 8]) = kpf[u];
-      *reinterpret_cast<bf16x8*>(&sV[buf][r * LD + cc * 8]) = vpf[u];
-    }
+    const size_t hs = size_t(p.hkv) * D, ho = size_t(kvh) * D;
+    tile_load_async<D, BN>(sK[buf], [&](int r) { return Kg + size_t(min(k0 + r, last)) * hs + ho; });
+    tile_load_async<D, BN>(sV[buf], [&](int r) { return Vg + size_t(min(k0 + r, last)) * hs + ho; });
   };
 
-  if (n_t > 0) {
-    fetch(0);
-    commit(0);
-  }
+  if (n_t > 0) fetch(0, 0);
 
   bf16x8 qreg[KS];
   {
@@ -103,11 +81,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   for (int db = 0; db < DB; ++db) oacc[db] = zero16();
   float m = -INFINITY;  // reference row maximum (scaled, log2 units)
   float lsum = 0.f;     // this lane's share of the row sum
+  wait_async();
   __syncthreads();
 
   for (int j = 0; j < n_t; ++j) {
     const int buf = j & 1;
-    if (j + 1 < n_t) fetch(j + 1);
+    if (j + 1 < n_t) fetch(j + 1, buf ^ 1);
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
@@ -120,8 +99,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       s[mb] = zero16();
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        s[mb] = mfma32(lds_read8(K, (mb * 32 + (lane & 31)) * LD + 16 * ks + 8 * half), qreg[ks],
-                       s[mb]);
+        s[mb] = mfma32(tread8<D>(K, mb * 32 + (lane & 31), 16 * ks + 8 * half), qreg[ks], s[mb]);
     }
     // mask keys past the range and, on diagonal tiles, keys after the query
     const bool diag = !rs && k0 >= ldiag;
@@ -170,9 +148,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       const int rb = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * half;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
-        oacc[db] = mfma32(lds_operand_tr(V, LD, rb, rb + 8, 32 * db, lane), pb, oacc[db]);
+        oacc[db] = mfma32(tread_tr<D>(V, rb, rb + 8, 32 * db, lane), pb, oacc[db]);
     }
-    if (j + 1 < n_t) commit(buf ^ 1);
+    wait_async();
     __syncthreads();
   }
 

@@ -8,6 +8,13 @@
 // ds_read_b64_tr_b16: within each group of 16 lanes, lane t addresses row
 // R0 + t/4, columns C0 + 4*(t%4) .. +3 of a row-major bf16 matrix, and
 // receives column C0 + t of rows R0 .. R0+3.
+// global_load_lds_dwordx4: lane i's 16 bytes land at the wave's LDS base
+// + 16*i.
+//
+// LDS tiles are unpadded row-major bf16 (D columns); the 16-byte chunk c of
+// row r is stored at chunk position c ^ swz(r). With that swizzle the 16-byte
+// row reads (eight rows per phase) and the 4-row transpose reads (two chunks
+// of four consecutive rows) both touch distinct banks.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -97,5 +104,50 @@ __device__ __forceinline__ bf16x8 pack8(const f32x16& c, int i0) {
   for (int j = 0; j < 8; ++j) r[j] = (__bf16)c[i0 + j];
   return r;
 }
+
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+// Element offset of (row r, column col) in a swizzled tile; col % 4 == 0.
+template <int D>
+__device__ __forceinline__ int toff(int r, int col) {
+  return r * D + ((((col >> 3) ^ swz(r)) << 3) | (col & 7));
+}
+
+// 8 consecutive bf16 of row r starting at column col (col % 8 == 0).
+template <int D>
+__device__ __forceinline__ bf16x8 tread8(const u16* T, int r, int col) {
+  return *reinterpret_cast<const bf16x8*>(T + toff<D>(r, col));
+}
+
+// MFMA operand holding X[k][nbase + l%32] of a swizzled tile for 8 values of
+// k taken as two runs of four rows, r0(l)..r0(l)+3 then r1(l)..r1(l)+3.
+template <int D>
+__device__ __forceinline__ bf16x8 tread_tr(const u16* T, int r0, int r1, int nbase, int lane) {
+  const int t = lane & 15;
+  const int col = nbase + 16 * ((lane >> 4) & 1) + 4 * (t & 3);
+  const bf16x4 a = lds_read_tr4(T, toff<D>(r0 + (t >> 2), col));
+  const bf16x4 b = lds_read_tr4(T, toff<D>(r1 + (t >> 2), col));
+  return cat8(a, b);
+}
+
+// Asynchronous copy of ROWS rows of D bf16 into a swizzled LDS tile, 256
+// threads; rowptr(r) is the global address of the row that goes to tile row
+// r. Completion: wait_async() then a barrier.
+template <int D, int ROWS, class RowPtr>
+__device__ __forceinline__ void tile_load_async(u16* T, RowPtr rowptr) {
+  constexpr int CH = D / 8;
+  static_assert((ROWS * CH) % 256 == 0, "tile must be a multiple of 256 chunks");
+#pragma unroll
+  for (int u = 0; u < ROWS * CH / 256; ++u) {
+    const int L = u * 256 + threadIdx.x;
+    const int r = L / CH;
+    const int c = (L % CH) ^ swz(r);
+    const u16* src = rowptr(r) + 8 * c;
+    u16* dst = T + (u * 256 + (threadIdx.x & ~63)) * 8;  // wave-uniform base
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void wait_async() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 }  // namespace fck

@@ -30,7 +30,7 @@ EXPORTS = [
     "fc_plan_stats", "fc_view_create", "fc_view_get_info", "fc_view_export", "fc_view_bind",
     "fc_view_destroy", "fc_workspace_size", "fc_kv_gather", "fc_attn_fwd",
     "fc_attn_fwd_partial", "fc_lse_merge", "fc_attn_bwd", "fc_bwd_preprocess",
-    "fc_attn_bwd_pass", "fc_last_error",
+    "fc_attn_bwd_pass", "fc_attn_bwd_dkdv", "fc_attn_bwd_dq", "fc_last_error",
 ]
 
 
@@ -93,6 +93,8 @@ def lib():
             "fc_attn_bwd": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P, C.c_size_t, P],
             "fc_bwd_preprocess": [P, P, P, P, P],
             "fc_attn_bwd_pass": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P],
+            "fc_attn_bwd_dkdv": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P],
+            "fc_attn_bwd_dq": [P, P, P, P, P, P, P, P, P, C.c_float, P, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -364,3 +366,32 @@ def fc_attn_bwd_pass(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do
         _ptr(dq, (tq, hq, d), f32, "dq"), _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"),
         _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
         _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), _stream()))
+
+
+def fc_attn_bwd_dkdv(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
+                     dk_loc, dv_loc, dk_recv, dv_recv):
+    import torch
+    i = view.info
+    bf, f32 = torch.bfloat16, torch.float32
+    tq, tr, hq, hkv, d = i["t_q"], i["t_recv"], i["hq"], i["hkv"], i["d"]
+    _check(lib().fc_attn_bwd_dkdv(
+        view.handle, _ptr(q, (tq, hq, d), bf, "q"), _ptr(k_loc, (tq, hkv, d), bf, "k_loc"),
+        _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
+        _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), _ptr(lse, (hq, tq), f32, "lse"),
+        _ptr(delta, (hq, tq), f32, "delta"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
+        _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"), _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"),
+        _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"), _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"),
+        _stream()))
+
+
+def fc_attn_bwd_dq(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq):
+    import torch
+    i = view.info
+    bf, f32 = torch.bfloat16, torch.float32
+    tq, tr, hq, hkv, d = i["t_q"], i["t_recv"], i["hq"], i["hkv"], i["d"]
+    _check(lib().fc_attn_bwd_dq(
+        view.handle, _ptr(q, (tq, hq, d), bf, "q"), _ptr(k_loc, (tq, hkv, d), bf, "k_loc"),
+        _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
+        _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), _ptr(lse, (hq, tq), f32, "lse"),
+        _ptr(delta, (hq, tq), f32, "delta"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
+        _ptr(dq, (tq, hq, d), f32, "dq"), _stream()))
