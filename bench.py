@@ -150,6 +150,8 @@ def main():
     dk_recv = torch.empty(tr, hkv, d, dtype=f32, device=dev)
     dv_recv = torch.empty_like(dk_recv)
     meta = torch.empty(int(info["meta_bytes"]) + 256, dtype=torch.uint8, device=dev)
+    no_ws = torch.empty(0, dtype=torch.uint8, device=dev)
+    dkdv_ws = torch.empty(view.workspace_size()[2], dtype=torch.uint8, device=dev)
     names = ["kv_gather", "attn_fwd_local", "attn_fwd_recv", "lse_merge", "bwd_preprocess",
              "attn_bwd_dkdv", "attn_bwd_dq"]
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
@@ -163,19 +165,22 @@ def main():
         ev[0].record()
         F.fc_kv_gather(v, k_pk, v_pk, k_loc, v_loc, k_recv, v_recv)
         ev[1].record()
-        F.fc_attn_fwd_partial(v, 0, q, k_loc, v_loc, 0.0, o_a, l_a)
-        ev[2].record()
         if tr:
+            F.fc_attn_fwd_partial(v, 0, q, k_loc, v_loc, 0.0, o_a, l_a)
+            ev[2].record()
             F.fc_attn_fwd_partial(v, 1, q, k_recv, v_recv, 0.0, o_b, l_b)
             ev[3].record()
             F.fc_lse_merge(o_a, l_a, o_b, l_b, o, None, lse)
         else:
-            raise SystemExit("bench.py: workload has no received KV; two-pass mode needs it")
+            # no received KV: the local pass alone writes the final O and LSE
+            F.fc_attn_fwd(v, q, k_loc, v_loc, k_recv, v_recv, 0.0, F.FC_TWO_PASS, o, None, lse, no_ws)
+            ev[2].record()
+            ev[3].record()
         ev[4].record()
         F.fc_bwd_preprocess(v, o, do, delta)
         ev[5].record()
         F.fc_attn_bwd_dkdv(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dk_loc,
-                           dv_loc, dk_recv, dv_recv)
+                           dv_loc, dk_recv, dv_recv, dkdv_ws)
         ev[6].record()
         F.fc_attn_bwd_dq(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq)
         ev[7].record()
@@ -210,7 +215,7 @@ def main():
         "kv_gather": ("hbm", 2 * 2 * kv_rows * hkv * d * 2),
         "attn_fwd_local": ("mfma", 4.0 * d * hq * info["pairs_loc"]),
         "attn_fwd_recv": ("mfma", 4.0 * d * hq * info["pairs_recv"]),
-        "lse_merge": ("hbm", tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4)),
+        "lse_merge": ("hbm", tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4) if tr else 0),
         "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4)),
         # dK/dV pass: S, dP, dV, dK (8d per pair); dQ pass: S, dP again and dQ (6d)
         "attn_bwd_dkdv": ("mfma", 8.0 * d * hq * pairs),
@@ -220,6 +225,9 @@ def main():
     for i, n in enumerate(names):
         kind, amount = work[n]
         t = acc[i] * 1e-3
+        if amount == 0 or acc[i] <= 0:
+            kernels[n] = {"ms": round(acc[i], 4), "skipped": "no received KV"}
+            continue
         if kind == "mfma":
             a = amount / t / 1e12
             kernels[n] = {"ms": round(acc[i], 4), "tflops": round(a, 1), "frac_bf16_peak": round(a / BF16_PEAK_TFLOPS, 4)}

@@ -144,6 +144,9 @@ typedef struct {
   int64_t n_fwd_local, n_fwd_recv, n_fwd_fused, n_bwd; /* work items */
   int64_t pairs_loc, pairs_recv; /* visible (query, key) pairs per head */
   int64_t meta_bytes;           /* device bytes fc_view_bind needs */
+  int64_t n_bwd_launch;         /* backward launch items after splitting long */
+  int64_t n_bwd_reduce;         /*   key tiles; key tiles split; partial slots */
+  int64_t n_bwd_slots;
 } fc_view_info;
 
 /* Build rank `rank`'s view of a validated plan (FC_ERR_PLAN otherwise) for
@@ -175,8 +178,10 @@ int fc_view_bind(fc_view view, void* dev_meta, size_t bytes, void* stream);
 
 void fc_view_destroy(fc_view view);
 
-/* Workspace bytes fc_attn_fwd (for `mode`) and fc_attn_bwd need. */
-int fc_workspace_size(fc_view view, int32_t mode, size_t* fwd_bytes, size_t* bwd_bytes);
+/* Workspace bytes fc_attn_fwd (for `mode`), fc_attn_bwd and, alone,
+ * fc_attn_bwd_dkdv / fc_attn_bwd_pass need (any pointer may be NULL). */
+int fc_workspace_size(fc_view view, int32_t mode, size_t* fwd_bytes, size_t* bwd_bytes,
+                      size_t* dkdv_bytes);
 
 /* ---------------------------------------------------------------- kernels */
 
@@ -227,18 +232,22 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
 int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta,
                       void* stream);
 /* The two kernels of fc_attn_bwd_pass, callable alone: the key-major
- * dK/dV pass (writes dk_*, dv_*) and the query-major dQ pass (writes dq). */
+ * dK/dV pass (writes dk_*, dv_*) and the query-major dQ pass (writes dq).
+ * Key tiles seen by very many query tiles are split across workgroups that
+ * write fp32 partials into ws, then summed in a fixed order, so dK/dV stay
+ * reproducible. ws: device, >= the dkdv_bytes of fc_workspace_size; may be
+ * NULL when that is 0 (no split key tile). */
 int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,
                      const void* dout, float scale, float* dk_loc, float* dv_loc, float* dk_recv,
-                     float* dv_recv, void* stream);
+                     float* dv_recv, void* ws, size_t ws_bytes, void* stream);
 int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                    const void* k_recv, const void* v_recv, const float* lse, const float* delta,
                    const void* dout, float scale, float* dq, void* stream);
 int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,
                      const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                     float* dk_recv, float* dv_recv, void* stream);
+                     float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes, void* stream);
 
 const char* fc_last_error(void);
 

@@ -43,7 +43,11 @@ FwdWs fwd_ws(const View& v, int32_t mode) {
   }
   return w;
 }
-size_t bwd_ws(const View& v) { return align_up(size_t(v.t_q()) * v.hq * sizeof(float)); }
+size_t delta_ws(const View& v) { return align_up(size_t(v.t_q()) * v.hq * sizeof(float)); }
+size_t part_ws(const View& v) {
+  return 2 * size_t(v.n_bwd_slots) * v.hkv * v.bn_bwd * v.d * sizeof(float);
+}
+size_t bwd_ws(const View& v) { return delta_ws(v) + part_ws(v); }
 
 fck::FwdParams fwd_params(const View& v, const int32_t* items, const int32_t* perm, int64_t n,
                           const void* q, const void* k_loc, const void* v_loc, const void* k_recv,
@@ -70,13 +74,15 @@ fck::FwdParams fwd_params(const View& v, const int32_t* items, const int32_t* pe
 
 extern "C" {
 
-int fc_workspace_size(fc_view view, int32_t mode, size_t* fwd_bytes, size_t* bwd_bytes) {
+int fc_workspace_size(fc_view view, int32_t mode, size_t* fwd_bytes, size_t* bwd_bytes,
+                      size_t* dkdv_bytes) {
   fc::clear_error();
   if (!view) return fail(FC_ERR_INVALID_ARG, "view is null");
   if (mode != FC_TWO_PASS && mode != FC_FUSED) return fail(FC_ERR_INVALID_ARG, "bad mode");
   const View& v = *reinterpret_cast<View*>(view);
   if (fwd_bytes) *fwd_bytes = fwd_ws(v, mode).total;
   if (bwd_bytes) *bwd_bytes = bwd_ws(v);
+  if (dkdv_bytes) *dkdv_bytes = part_ws(v);
   return FC_OK;
 }
 
@@ -219,7 +225,7 @@ int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delt
 int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,
                      const void* dout, float scale, float* dk_loc, float* dv_loc, float* dk_recv,
-                     float* dv_recv, void* stream) {
+                     float* dv_recv, void* ws, size_t ws_bytes, void* stream) {
   fc::clear_error();
   View* v;
   if (int rc = check_view(view, v)) return rc;
@@ -227,6 +233,10 @@ int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void*
   if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dk_loc || !dv_loc ||
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  const size_t need = part_ws(*v);
+  if (need && (!ws || ws_bytes < need))
+    return fail(FC_ERR_WORKSPACE, "dK/dV workspace of " + std::to_string(ws_bytes) +
+                                      " bytes, need " + std::to_string(need));
   const int32_t* m = v->dev_meta;
   fck::BwdParams p{};
   p.q = static_cast<const uint16_t*>(q);
@@ -237,10 +247,12 @@ int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void*
   p.v_loc = static_cast<const uint16_t*>(v_loc);
   p.k_recv = static_cast<const uint16_t*>(k_recv);
   p.v_recv = static_cast<const uint16_t*>(v_recv);
-  p.items = m + v->off.bwd;
-  p.perm = m + v->off.perm_bwd;
+  p.items = m + v->off.bwd_launch;
+  p.perm = m + v->off.perm_bwd_launch;
   p.lim = m + v->off.lim;
-  p.n_items = int32_t(v->bwd.size() / 8);
+  p.n_items = int32_t(v->bwd_launch.size() / 8);
+  p.part_k = static_cast<float*>(ws);
+  p.part_v = need ? reinterpret_cast<float*>(static_cast<char*>(ws) + need / 2) : nullptr;
   p.hq = v->hq;
   p.hkv = v->hkv;
   p.group = v->hq / v->hkv;
@@ -250,8 +262,12 @@ int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void*
   p.dk_recv = dk_recv;
   p.dv_recv = dv_recv;
   p.t_q = v->t_q();
-  return hip_status(fck::launch_bwd(p, v->d, reinterpret_cast<hipStream_t>(stream)),
-                    "attn_bwd dK/dV launch");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (int rc = hip_status(fck::launch_bwd(p, v->d, s), "attn_bwd dK/dV launch")) return rc;
+  return hip_status(fck::launch_bwd_reduce(m + v->off.bwd_reduce, int32_t(v->bwd_reduce.size() / 8),
+                                           p.part_k, p.part_v, v->hkv, v->d, dk_loc, dv_loc,
+                                           dk_recv, dv_recv, s),
+                    "attn_bwd reduce launch");
 }
 
 int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v_loc,
@@ -292,14 +308,14 @@ int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v
 int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,
                      const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                     float* dk_recv, float* dv_recv, void* stream) {
+                     float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes, void* stream) {
   fc::clear_error();
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
   if (!dq) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
   if (int rc = fc_attn_bwd_dkdv(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
-                                dk_loc, dv_loc, dk_recv, dv_recv, stream))
+                                dk_loc, dv_loc, dk_recv, dv_recv, ws, ws_bytes, stream))
     return rc;
   return fc_attn_bwd_dq(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq,
                         stream);
@@ -324,8 +340,10 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
   if (int rc = fc_bwd_preprocess(view, o, dout, delta, stream)) return rc;
+  const size_t dbytes = delta_ws(*v);
   return fc_attn_bwd_pass(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq,
-                          dk_loc, dv_loc, dk_recv, dv_recv, stream);
+                          dk_loc, dv_loc, dk_recv, dv_recv, static_cast<char*>(ws) + dbytes,
+                          ws_bytes - dbytes, stream);
 }
 
 }  // extern "C"

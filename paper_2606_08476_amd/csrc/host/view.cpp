@@ -119,6 +119,49 @@ void View::build_tiles() {
   std::vector<int64_t> bc(bwd.size() / 8);
   for (size_t i = 0; i < bc.size(); ++i) bc[i] = ceil_div(bwd[8 * i + 3] - bwd[8 * i + 2], bm_bwd);
   perm_bwd = lpt_order(bc);
+  build_bwd_launch();
+}
+
+// Split key tiles whose query range is much longer than a fair share of the
+// backward's work: with about 512 workgroups resident at a time (256 CUs, two
+// per CU), an item longer than total/512 iterations would finish after
+// everything else. Its query tiles are cut into equal parts; each part
+// writes fp32 partial dK/dV to its own slot and a reduce pass sums the parts
+// in slot order (deterministic).
+void View::build_bwd_launch() {
+  constexpr int64_t kSlotsResident = 512;
+  const int64_t G = hq / hkv;
+  const size_t n = bwd.size() / 8;
+  int64_t total = 0;
+  for (size_t i = 0; i < n; ++i) total += ceil_div(bwd[8 * i + 3] - bwd[8 * i + 2], bm_bwd) * G;
+  const int64_t cap = std::max<int64_t>(16, (total * hkv + kSlotsResident - 1) / kSlotsResident);
+  bwd_launch.clear();
+  bwd_reduce.clear();
+  n_bwd_slots = 0;
+  std::vector<int64_t> cost;
+  for (size_t i = 0; i < n; ++i) {
+    const int32_t* it = &bwd[8 * i];
+    const int32_t ntile = ceil_div(it[3] - it[2], bm_bwd);
+    const int32_t parts = int32_t(std::max<int64_t>(1, (int64_t(ntile) * G + cap - 1) / cap));
+    if (parts == 1) {
+      bwd_launch.insert(bwd_launch.end(), {it[0], it[1], it[2], it[3], it[4], it[5], it[6], -1});
+      cost.push_back(int64_t(ntile) * G);
+      continue;
+    }
+    const int32_t per = ceil_div(ntile, parts);
+    bwd_reduce.insert(bwd_reduce.end(), {it[5], it[0], it[1], n_bwd_slots, 0, 0, 0, 0});
+    int32_t made = 0;
+    for (int32_t t = 0; t < ntile; t += per) {
+      const int32_t a = it[2] + t * bm_bwd;
+      const int32_t b = std::min(it[3], it[2] + (t + per) * bm_bwd);
+      bwd_launch.insert(bwd_launch.end(), {it[0], it[1], a, b, it[4], it[5], it[6], n_bwd_slots});
+      cost.push_back(int64_t(std::min(per, ntile - t)) * G);
+      ++n_bwd_slots;
+      ++made;
+    }
+    bwd_reduce[bwd_reduce.size() - 4] = made;
+  }
+  perm_bwd_launch = lpt_order(cost);
 }
 
 void View::build_meta() {
@@ -140,6 +183,9 @@ void View::build_meta() {
   off.q_gpos = put(q_gpos);
   off.recv_gpos = put(recv_gpos);
   off.lim = put(lim);
+  off.bwd_launch = put(bwd_launch);
+  off.perm_bwd_launch = put(perm_bwd_launch);
+  off.bwd_reduce = put(bwd_reduce);
   if (meta.empty()) meta.resize(64, 0);
 }
 
@@ -251,6 +297,9 @@ int fc_view_get_info(fc_view view, fc_view_info* out) {
   out->pairs_loc = v.pairs_loc;
   out->pairs_recv = v.pairs_recv;
   out->meta_bytes = int64_t(v.meta.size() * sizeof(int32_t));
+  out->n_bwd_launch = int64_t(v.bwd_launch.size() / 8);
+  out->n_bwd_reduce = int64_t(v.bwd_reduce.size() / 8);
+  out->n_bwd_slots = v.n_bwd_slots;
   return FC_OK;
 }
 

@@ -21,6 +21,12 @@ struct View {
   // work lists, 8 int32 per item (layout documented in flashcp.h)
   std::vector<int32_t> fwd_local, fwd_recv, fwd_fused, bwd;
   std::vector<int32_t> perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
+  // backward launch list: the key-major items with long query ranges split
+  // into parts that write partial dK/dV (last field: partial slot, -1 for a
+  // direct write), and one reduce entry per split key tile
+  // (src, k0, k1, first slot, slot count, 0, 0, 0)
+  std::vector<int32_t> bwd_launch, perm_bwd_launch, bwd_reduce;
+  int32_t n_bwd_slots = 0;
 
   // device blob: every table above that a kernel reads, int32, sections
   // aligned to 256 bytes; `off` holds section offsets in int32 elements
@@ -29,12 +35,14 @@ struct View {
     int64_t fwd_local, fwd_recv, fwd_fused, bwd;
     int64_t perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
     int64_t q_gpos, recv_gpos, lim;
+    int64_t bwd_launch, perm_bwd_launch, bwd_reduce;
   } off{};
   const int32_t* dev_meta = nullptr;        // set by fc_view_bind
 
   int32_t t_q() const { return int32_t(q_gpos.size()); }
   int32_t t_recv() const { return int32_t(recv_gpos.size()); }
   void build_tiles();
+  void build_bwd_launch();
   void build_meta();
 };
 

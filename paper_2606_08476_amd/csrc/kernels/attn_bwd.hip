@@ -38,7 +38,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   const int half = lane >> 5;
   const int b = blockIdx.x;
   const int kvh = b % p.hkv;
-  const int32_t* it = p.items + 8 * p.perm[b / p.hkv];
+  const int32_t* it = p.items + 8 * p.perm[b / p.hkv];  // launch list
   const int k0 = it[0], k1 = it[1], q0 = it[2], q1 = it[3], qfull = it[4], src = it[5];
   const u16* Kg = src ? p.k_recv : p.k_loc;
   const u16* Vg = src ? p.v_recv : p.v_loc;
@@ -47,7 +47,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   const size_t kvs = size_t(p.hkv) * D, kvo = size_t(kvh) * D;
 
   // key tile (rows past k1 repeat the last key; they are masked)
-  tile_load_async<D, BN>(sK, [&](int r) { return Kg + size_t(min(k0 + r, k1 - 1)) * kvs + kvo; });
+  TileLoader<D, BN>(p.hkv * D).load(sK, Kg + size_t(k0) * kvs + kvo, k1 - k0);
   const int krow = 32 * wave + (lane & 31);  // this lane's key within the tile
   const int kidx = k0 + krow;
   const bool kvalid = kidx < k1;
@@ -66,12 +66,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   // next iteration: Q/dO tiles straight into LDS, LSE/D/limit via registers
   float lpf = 0.f, dpf = 0.f;
   int mpf = 0;
+  const TileLoader<D, BM> ldq(p.hq * D);
   auto fetch = [&](int i_, int buf) {
     const int h = kvh * p.group + i_ / ntile;
     const int t0 = q0 + (i_ % ntile) * BM;
-    const size_t qs = size_t(p.hq) * D, qo = size_t(h) * D;
-    tile_load_async<D, BM>(sQ[buf], [&](int r) { return p.q + size_t(min(t0 + r, q1 - 1)) * qs + qo; });
-    tile_load_async<D, BM>(sO[buf], [&](int r) { return p.dout + size_t(min(t0 + r, q1 - 1)) * qs + qo; });
+    const size_t base = (size_t(t0) * p.hq + h) * D;
+    ldq.load(sQ[buf], p.q + base, q1 - t0);
+    ldq.load(sO[buf], p.dout + base, q1 - t0);
     if (threadIdx.x < BM) {
       const int qi = min(t0 + int(threadIdx.x), q1 - 1);
       lpf = p.lse[(size_t)h * p.t_q + qi];
@@ -95,6 +96,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   }
   const bool kfull = k1 - k0 == BN;
   const float sl2 = p.scale * kLog2e;
+  const int qb = row_base<D>(0, lane), kb = row_base<D>(32 * wave, lane), trb = tr_base<D>(lane);
 
   if (n_it > 0) {
     fetch(0, 0);
@@ -114,9 +116,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
     f32x16 sacc = zero16(), dpacc = zero16();
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const int col = 16 * ks + 8 * half;
-      sacc = mfma32(tread8<D>(Q, lane & 31, col), tread8<D>(sK, krow, col), sacc);
-      dpacc = mfma32(tread8<D>(O, lane & 31, col), vreg[ks], dpacc);
+      sacc = mfma32(tread8_ks<D>(Q, qb, ks), tread8_ks<D>(sK, kb, ks), sacc);
+      dpacc = mfma32(tread8_ks<D>(O, qb, ks), vreg[ks], dpacc);
     }
     // this lane's 16 query rows are 8g + 4*half + 0..3, g = 0..3
     const bool diag = t0 < qfull;
@@ -147,11 +148,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
     for (int kh = 0; kh < 2; ++kh) {
       const bf16x8 pa = pack8(sacc, 8 * kh);
       const bf16x8 sa = pack8(dpacc, 8 * kh);
-      const int rb = 16 * kh + 4 * half;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        dv[db] = mfma32(pa, tread_tr<D>(O, rb, rb + 8, 32 * db, lane), dv[db]);
-        dk[db] = mfma32(sa, tread_tr<D>(Q, rb, rb + 8, 32 * db, lane), dk[db]);
+        dv[db] = mfma32(pa, tread_tr2<D>(O, trb, 16 * kh, db), dv[db]);
+        dk[db] = mfma32(sa, tread_tr2<D>(Q, trb, 16 * kh, db), dk[db]);
       }
     }
     wait_async();
@@ -159,15 +159,28 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
     __syncthreads();
   }
 
+  // dK/dV of this tile, or of this part of a split tile (partial slot)
+  const int slot = it[7];
+  float* outK = dKg;
+  float* outV = dVg;
+  size_t rs = size_t(p.hkv) * D, base = size_t(kvh) * D;
+  int r0 = k0;
+  if (slot >= 0) {
+    outK = p.part_k;
+    outV = p.part_v;
+    rs = D;
+    base = (size_t(slot) * p.hkv + kvh) * BN * D;
+    r0 = 0;
+  }
 #pragma unroll
   for (int db = 0; db < DB; ++db) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int kr = k0 + 32 * wave + 8 * (i >> 2) + 4 * half + (i & 3);
-      if (kr < k1) {
-        const size_t g = ((size_t)kr * p.hkv + kvh) * D + 32 * db + (lane & 31);
-        dKg[g] = p.scale * dk[db][i];
-        dVg[g] = dv[db][i];
+      const int r = 32 * wave + 8 * (i >> 2) + 4 * half + (i & 3);
+      if (k0 + r < k1) {
+        const size_t g = base + size_t(r0 + r) * rs + 32 * db + (lane & 31);
+        outK[g] = p.scale * dk[db][i];
+        outV[g] = dv[db][i];
       }
     }
   }

@@ -46,15 +46,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
   const int n_r = (r1 - r0 + BN - 1) / BN;
   const int n_t = n_r + (l1 - l0 + BN - 1) / BN;
 
+  const TileLoader<D, BN> ld(p.hkv * D);
   auto fetch = [&](int j, int buf) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
-    const int last = (rs ? r1 : l1) - 1;
-    const u16* Kg = rs ? p.k_recv : p.k_loc;
-    const u16* Vg = rs ? p.v_recv : p.v_loc;
-    const size_t hs = size_t(p.hkv) * D, ho = size_t(kvh) * D;
-    tile_load_async<D, BN>(sK[buf], [&](int r) { return Kg + size_t(min(k0 + r, last)) * hs + ho; });
-    tile_load_async<D, BN>(sV[buf], [&](int r) { return Vg + size_t(min(k0 + r, last)) * hs + ho; });
+    const int hi = rs ? r1 : l1;
+    const size_t base = (size_t(k0) * p.hkv + kvh) * D;
+    ld.load(sK[buf], (rs ? p.k_recv : p.k_loc) + base, hi - k0);
+    ld.load(sV[buf], (rs ? p.v_recv : p.v_loc) + base, hi - k0);
   };
 
   if (n_t > 0) fetch(0, 0);
@@ -74,6 +73,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
     }
   }
 
+  const int kb0 = row_base<D>(0, lane), kb1 = row_base<D>(32, lane), ktb = tr_base<D>(lane);
   f32x16 dq[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
@@ -89,18 +89,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
     const u16* K = sK[buf];
     const u16* V = sV[buf];
 
-    f32x16 s[2], dp[2];
+    // four independent accumulator chains, interleaved
+    f32x16 s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      s[mb] = zero16();
-      dp[mb] = zero16();
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int row = mb * 32 + (lane & 31), col = 16 * ks + 8 * half;
-        s[mb] = mfma32(tread8<D>(K, row, col), qreg[ks], s[mb]);
-        dp[mb] = mfma32(tread8<D>(V, row, col), oreg[ks], dp[mb]);
+      for (int mb = 0; mb < 2; ++mb) {
+        s[mb] = mfma32(tread8_ks<D>(K, mb ? kb1 : kb0, ks), qreg[ks], s[mb]);
+        dp[mb] = mfma32(tread8_ks<D>(V, mb ? kb1 : kb0, ks), oreg[ks], dp[mb]);
       }
-    }
     const bool diag = !rs && k0 >= ldiag;
     const bool edge = diag || k0 + BN > hi;
 #pragma unroll
@@ -119,10 +116,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const bf16x8 sb = pack8(dp[kk >> 1], 8 * (kk & 1));
-      const int rb = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * half;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
-        dq[db] = mfma32(tread_tr<D>(K, rb, rb + 8, 32 * db, lane), sb, dq[db]);
+        dq[db] = mfma32(tread_tr2<D>(K, ktb, 16 * kk, db), sb, dq[db]);
     }
     wait_async();
     __syncthreads();

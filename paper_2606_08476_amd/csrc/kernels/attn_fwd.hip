@@ -55,15 +55,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
   // async load of key tile j into buffer `buf`; rows past the range repeat
   // the last row (finite data; those keys are masked)
+  const TileLoader<D, BN> ld(p.hkv * D);
   auto fetch = [&](int j, int buf) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
-    const int last = (rs ? r1 : l1) - 1;
-    const u16* Kg = rs ? p.k_recv : p.k_loc;
-    const u16* Vg = rs ? p.v_recv : p.v_loc;
-    const size_t hs = size_t(p.hkv) * D, ho = size_t(kvh) * D;
-    tile_load_async<D, BN>(sK[buf], [&](int r) { return Kg + size_t(min(k0 + r, last)) * hs + ho; });
-    tile_load_async<D, BN>(sV[buf], [&](int r) { return Vg + size_t(min(k0 + r, last)) * hs + ho; });
+    const int hi = rs ? r1 : l1;
+    const size_t base = (size_t(k0) * p.hkv + kvh) * D;
+    ld.load(sK[buf], (rs ? p.k_recv : p.k_loc) + base, hi - k0);
+    ld.load(sV[buf], (rs ? p.v_recv : p.v_loc) + base, hi - k0);
   };
 
   if (n_t > 0) fetch(0, 0);
@@ -76,6 +75,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       qreg[ks] = qvalid ? *reinterpret_cast<const bf16x8*>(qp + 16 * ks) : zero8();
   }
 
+  const int kb0 = row_base<D>(0, lane), kb1 = row_base<D>(32, lane), vtb = tr_base<D>(lane);
   f32x16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) oacc[db] = zero16();
@@ -93,14 +93,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     const u16* K = sK[buf];
     const u16* V = sV[buf];
 
-    f32x16 s[2];
+    // two independent accumulator chains, interleaved
+    f32x16 s[2] = {zero16(), zero16()};
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      s[mb] = zero16();
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        s[mb] = mfma32(tread8<D>(K, mb * 32 + (lane & 31), 16 * ks + 8 * half), qreg[ks], s[mb]);
-    }
+      for (int mb = 0; mb < 2; ++mb)
+        s[mb] = mfma32(tread8_ks<D>(K, mb ? kb1 : kb0, ks), qreg[ks], s[mb]);
     // mask keys past the range and, on diagonal tiles, keys after the query
     const bool diag = !rs && k0 >= ldiag;
     if (diag || k0 + BN > hi) {
@@ -145,10 +144,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const bf16x8 pb = pack8(s[kk >> 1], 8 * (kk & 1));
-      const int rb = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * half;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
-        oacc[db] = mfma32(tread_tr<D>(V, rb, rb + 8, 32 * db, lane), pb, oacc[db]);
+        oacc[db] = mfma32(tread_tr2<D>(V, vtb, 16 * kk, db), pb, oacc[db]);
     }
     wait_async();
     __syncthreads();

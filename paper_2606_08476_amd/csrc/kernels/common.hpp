@@ -12,9 +12,10 @@
 // + 16*i.
 //
 // LDS tiles are unpadded row-major bf16 (D columns); the 16-byte chunk c of
-// row r is stored at chunk position c ^ swz(r). With that swizzle the 16-byte
-// row reads (eight rows per phase) and the 4-row transpose reads (two chunks
-// of four consecutive rows) both touch distinct banks.
+// row r is stored at chunk position c ^ swz<D>(r). The LDS serves 256 bytes
+// (64 banks) per cycle; with the swizzle both access patterns fill them
+// without conflicts: 16-byte row reads (16 lanes = 16 consecutive rows, one
+// chunk) and transpose reads (32 lanes = 4 consecutive rows x 4 chunks).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -105,12 +106,18 @@ __device__ __forceinline__ bf16x8 pack8(const f32x16& c, int i0) {
   return r;
 }
 
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128)
+    return ((r & 3) << 2) | ((r >> 2) & 3);           // one row per 256 bytes
+  else
+    return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);    // two rows per 256 bytes
+}
 
 // Element offset of (row r, column col) in a swizzled tile; col % 4 == 0.
 template <int D>
 __device__ __forceinline__ int toff(int r, int col) {
-  return r * D + ((((col >> 3) ^ swz(r)) << 3) | (col & 7));
+  return r * D + ((((col >> 3) ^ swz<D>(r)) << 3) | (col & 7));
 }
 
 // 8 consecutive bf16 of row r starting at column col (col % 8 == 0).
@@ -130,23 +137,75 @@ __device__ __forceinline__ bf16x8 tread_tr(const u16* T, int r0, int r1, int nba
   return cat8(a, b);
 }
 
-// Asynchronous copy of ROWS rows of D bf16 into a swizzled LDS tile, 256
-// threads; rowptr(r) is the global address of the row that goes to tile row
-// r. Completion: wait_async() then a barrier.
-template <int D, int ROWS, class RowPtr>
-__device__ __forceinline__ void tile_load_async(u16* T, RowPtr rowptr) {
-  constexpr int CH = D / 8;
-  static_assert((ROWS * CH) % 256 == 0, "tile must be a multiple of 256 chunks");
-#pragma unroll
-  for (int u = 0; u < ROWS * CH / 256; ++u) {
-    const int L = u * 256 + threadIdx.x;
-    const int r = L / CH;
-    const int c = (L % CH) ^ swz(r);
-    const u16* src = rowptr(r) + 8 * c;
-    u16* dst = T + (u * 256 + (threadIdx.x & ~63)) * 8;  // wave-uniform base
-    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
-  }
+// Cheap addressing of the swizzled tiles: every MFMA operand read below is a
+// per-lane base XOR a compile-time constant, plus a constant row offset.
+//
+// Row reads: rows base_row + (lane & 31) (base_row a multiple of 32), 8
+// columns from 16*ks + 8*(lane/32); offset = row_base ^ (ks << 4).
+template <int D>
+__device__ __forceinline__ int row_base(int base_row, int lane) {
+  const int r = base_row + (lane & 31), half = lane >> 5, f = swz<D>(r);
+  return (r * D) | ((half ^ (f & 1)) << 3) | ((f >> 1) << 4);
 }
+template <int D>
+__device__ __forceinline__ bf16x8 tread8_ks(const u16* T, int base, int ks) {
+  return *reinterpret_cast<const bf16x8*>(T + (base ^ (ks << 4)));
+}
+
+// Transpose reads forming an operand with k = rows R + 4*(lane/32) + 0..3 and
+// R + 8 + 4*(lane/32) + 0..3 (R a multiple of 16) and n = columns
+// 32*db + (lane % 32); tr_base is per lane, R and db compile-time.
+template <int D>
+__device__ __forceinline__ int tr_base(int lane) {
+  const int half = lane >> 5, t = lane & 15, g = (lane >> 4) & 1;
+  const int t4 = D == 128 ? ((t >> 2) << 2) : (((t >> 3) & 1) << 2);
+  const int x = (2 * g + ((t & 3) >> 1)) ^ half;
+  return ((4 * half + (t >> 2)) * D + (t & 1) * 4) | (x << 3) | (t4 << 3);
+}
+template <int D>
+__device__ __forceinline__ bf16x8 tread_tr2(const u16* T, int base, int R, int db) {
+  const bf16x4 a = lds_read_tr4(T, (base ^ (db << 5)) + R * D);
+  const bf16x4 b = lds_read_tr4(T, (base ^ ((db << 5) | 16)) + (R + 8) * D);
+  return cat8(a, b);
+}
+
+// Asynchronous copies of ROWS x D bf16 tiles (rows row_stride elements apart
+// in HBM) into a swizzled LDS tile, 256 threads. Each thread's chunk offsets
+// are computed once; a load is then one base address plus those offsets.
+// Rows at or past `nvalid` repeat row nvalid-1 (finite data for masked
+// rows, no read past the range). Completion: wait_async() then a barrier.
+template <int D, int ROWS>
+struct TileLoader {
+  static constexpr int CH = D / 8;
+  static constexpr int N = ROWS * CH / 256;
+  static_assert((ROWS * CH) % 256 == 0, "tile must be a multiple of 256 chunks");
+  int off[N];
+  int row_stride;
+
+  __device__ __forceinline__ explicit TileLoader(int stride) : row_stride(stride) {
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+      const int L = u * 256 + threadIdx.x;
+      const int r = L / CH;
+      off[u] = r * stride + 8 * ((L % CH) ^ swz<D>(r));
+    }
+  }
+
+  __device__ __forceinline__ void load(u16* T, const u16* g, int nvalid) const {
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+      int o = off[u];
+      if (nvalid < ROWS) {  // uniform: only the last, ragged tile of a range
+        const int L = u * 256 + threadIdx.x;
+        const int r = L / CH;
+        if (r >= nvalid) o = (nvalid - 1) * row_stride + 8 * ((L % CH) ^ swz<D>(r));
+      }
+      u16* dst = T + (u * 256 + (threadIdx.x & ~63)) * 8;  // wave-uniform base
+      __builtin_amdgcn_global_load_lds(g + o, (__attribute__((address_space(3))) void*)dst, 16,
+                                       0, 0);
+    }
+  }
+};
 
 __device__ __forceinline__ void wait_async() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 

@@ -90,6 +90,40 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const u16* __restrict__ o,
   }
 }
 
+// Sum of the partial dK/dV of a split key tile, in slot order. One
+// workgroup per (split tile, KV head); entries are (src, k0, k1, first slot,
+// slot count, 0, 0, 0); partial slots hold 128 rows of d values per KV head.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(const int32_t* __restrict__ entries,
+                                                         const float* __restrict__ pk,
+                                                         const float* __restrict__ pv, int32_t hkv,
+                                                         float* dk_loc, float* dv_loc,
+                                                         float* dk_recv, float* dv_recv) {
+  constexpr int BN = 128, C4 = D / 4;
+  const int kvh = blockIdx.x % hkv;
+  const int32_t* e = entries + 8 * (blockIdx.x / hkv);
+  const int src = e[0], k0 = e[1], k1 = e[2], s0 = e[3], ns = e[4];
+  float* dk = src ? dk_recv : dk_loc;
+  float* dv = src ? dv_recv : dv_loc;
+  for (int idx = threadIdx.x; idx < (k1 - k0) * C4; idx += 256) {
+    const int r = idx / C4, c = idx % C4;
+    f32x4 ak = {0.f, 0.f, 0.f, 0.f}, av = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < ns; ++s) {
+      const size_t o = ((size_t(s0 + s) * hkv + kvh) * BN + r) * D;
+      const f32x4 x = reinterpret_cast<const f32x4*>(pk + o)[c];
+      const f32x4 y = reinterpret_cast<const f32x4*>(pv + o)[c];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        ak[j] += x[j];
+        av[j] += y[j];
+      }
+    }
+    const size_t g = (size_t(k0 + r) * hkv + kvh) * D;
+    reinterpret_cast<f32x4*>(dk + g)[c] = ak;
+    reinterpret_cast<f32x4*>(dv + g)[c] = av;
+  }
+}
+
 static unsigned grid_for(int64_t threads) {
   const int64_t b = (threads + 255) / 256;
   return unsigned(b < 1 ? 1 : b);
@@ -123,6 +157,22 @@ hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o
   else if (d == 128)
     hipLaunchKernelGGL(lse_merge_kernel<128>, dim3(grid_for(rows * 32)), dim3(256), 0, s, o_a,
                        lse_a, o_b, lse_b, t, h, o_bf16, o_f32, lse_out);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_reduce(const int32_t* entries, int32_t n, const float* part_k,
+                             const float* part_v, int32_t hkv, int32_t d, float* dk_loc,
+                             float* dv_loc, float* dk_recv, float* dv_recv, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const dim3 grid(unsigned(n) * hkv), block(256);
+  if (d == 64)
+    hipLaunchKernelGGL(bwd_reduce_kernel<64>, grid, block, 0, s, entries, part_k, part_v, hkv,
+                       dk_loc, dv_loc, dk_recv, dv_recv);
+  else if (d == 128)
+    hipLaunchKernelGGL(bwd_reduce_kernel<128>, grid, block, 0, s, entries, part_k, part_v, hkv,
+                       dk_loc, dv_loc, dk_recv, dv_recv);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

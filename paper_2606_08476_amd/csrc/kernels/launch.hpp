@@ -34,9 +34,11 @@ struct BwdParams {
   const uint16_t* v_loc;
   const uint16_t* k_recv;
   const uint16_t* v_recv;
-  const int32_t* items;     // 8 int32 per item: k0 k1 q0 q1 qfull src seg 0
+  const int32_t* items;     // 8 int32 per item: k0 k1 q0 q1 qfull src seg slot
   const int32_t* perm;
   const int32_t* lim;       // [t_q] receive index end per query
+  float* part_k;            // [slots, hkv, 128, d] partial dK/dV of split key tiles
+  float* part_v;
   int32_t n_items;
   int32_t hq, hkv, group;
   float scale;
@@ -69,6 +71,9 @@ hipError_t launch_fwd(const FwdParams& p, int d, int heads_per_tile, bool final_
                       hipStream_t s);
 hipError_t launch_bwd_dq(const DqParams& p, int d, int heads_per_tile, hipStream_t s);
 hipError_t launch_bwd(const BwdParams& p, int d, hipStream_t s);
+hipError_t launch_bwd_reduce(const int32_t* entries, int32_t n, const float* part_k,
+                             const float* part_v, int32_t hkv, int32_t d, float* dk_loc,
+                             float* dv_loc, float* dk_recv, float* dv_recv, hipStream_t s);
 hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta,
                                  int32_t t, int32_t h, int32_t d, hipStream_t s);
 hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o_b,

@@ -52,7 +52,8 @@ class ViewInfo(C.Structure):
         ("pad_", C.c_int32),
         ("n_fwd_local", C.c_int64), ("n_fwd_recv", C.c_int64), ("n_fwd_fused", C.c_int64),
         ("n_bwd", C.c_int64), ("pairs_loc", C.c_int64), ("pairs_recv", C.c_int64),
-        ("meta_bytes", C.c_int64),
+        ("meta_bytes", C.c_int64), ("n_bwd_launch", C.c_int64), ("n_bwd_reduce", C.c_int64),
+        ("n_bwd_slots", C.c_int64),
     ]
 
     def as_dict(self):
@@ -85,15 +86,16 @@ def lib():
             "fc_view_get_info": [P, C.POINTER(ViewInfo)],
             "fc_view_export": [P] + [I32P] * 11,
             "fc_view_bind": [P, P, C.c_size_t, P],
-            "fc_workspace_size": [P, C.c_int32, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)],
+            "fc_workspace_size": [P, C.c_int32, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t),
+                                  C.POINTER(C.c_size_t)],
             "fc_kv_gather": [P, P, P, C.c_int64, P, P, P, P, P],
             "fc_attn_fwd": [P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, C.c_size_t, P],
             "fc_attn_fwd_partial": [P, C.c_int32, P, P, P, C.c_float, P, P, P],
             "fc_lse_merge": [P, P, P, P, C.c_int32, C.c_int32, C.c_int32, P, P, P, P],
             "fc_attn_bwd": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P, C.c_size_t, P],
             "fc_bwd_preprocess": [P, P, P, P, P],
-            "fc_attn_bwd_pass": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P],
-            "fc_attn_bwd_dkdv": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P],
+            "fc_attn_bwd_pass": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P, C.c_size_t, P],
+            "fc_attn_bwd_dkdv": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, C.c_size_t, P],
             "fc_attn_bwd_dq": [P, P, P, P, P, P, P, P, P, C.c_float, P, P],
         }
         for name, args in sig.items():
@@ -238,9 +240,10 @@ class View:
         return self
 
     def workspace_size(self, mode: int = FC_TWO_PASS):
-        f, b = C.c_size_t(0), C.c_size_t(0)
-        _check(lib().fc_workspace_size(self.handle, mode, C.byref(f), C.byref(b)))
-        return f.value, b.value
+        """(forward bytes, backward bytes, dK/dV-pass bytes)."""
+        f, b, k = C.c_size_t(0), C.c_size_t(0), C.c_size_t(0)
+        _check(lib().fc_workspace_size(self.handle, mode, C.byref(f), C.byref(b), C.byref(k)))
+        return f.value, b.value, k.value
 
     def close(self):
         if getattr(self, "_h", None) is not None:
@@ -352,8 +355,14 @@ def fc_bwd_preprocess(view: View, o, dout, delta):
         _ptr(delta, (hq, tq), torch.float32, "delta"), _stream()))
 
 
+def _ws(ws):
+    if ws is None or ws.numel() == 0:
+        return None, 0
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
 def fc_attn_bwd_pass(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
-                     dq, dk_loc, dv_loc, dk_recv, dv_recv):
+                     dq, dk_loc, dv_loc, dk_recv, dv_recv, ws=None):
     import torch
     i = view.info
     bf, f32 = torch.bfloat16, torch.float32
@@ -365,11 +374,11 @@ def fc_attn_bwd_pass(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do
         _ptr(delta, (hq, tq), f32, "delta"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
         _ptr(dq, (tq, hq, d), f32, "dq"), _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"),
         _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
-        _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), _stream()))
+        _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), *_ws(ws), _stream()))
 
 
 def fc_attn_bwd_dkdv(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
-                     dk_loc, dv_loc, dk_recv, dv_recv):
+                     dk_loc, dv_loc, dk_recv, dv_recv, ws=None):
     import torch
     i = view.info
     bf, f32 = torch.bfloat16, torch.float32
@@ -381,7 +390,7 @@ def fc_attn_bwd_dkdv(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do
         _ptr(delta, (hq, tq), f32, "delta"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
         _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"), _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"),
         _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"), _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"),
-        _stream()))
+        *_ws(ws), _stream()))
 
 
 def fc_attn_bwd_dq(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq):

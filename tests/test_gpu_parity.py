@@ -70,7 +70,7 @@ class Run:
         self.o = torch.empty(tq, hq, d, dtype=bf, device=dev)
         self.o32 = torch.empty(tq, hq, d, dtype=torch.float32, device=dev)
         self.lse = torch.empty(hq, tq, dtype=torch.float32, device=dev)
-        fws, bws = self.v.workspace_size(mode)
+        fws, bws, _ = self.v.workspace_size(mode)
         ws = torch.empty(max(fws, 1), dtype=torch.uint8, device=dev)
         F.fc_attn_fwd(self.v, self.q, self.k_loc, self.v_loc, self.k_recv, self.v_recv, 0.0, mode,
                       self.o, self.o32, self.lse, ws)

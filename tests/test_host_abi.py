@@ -171,14 +171,16 @@ def test_kernel_calls_rejected_before_launch():
     assert lib.fc_kv_gather(h, 1, 1, 128, 1, 1, 1, 1, None) == -5
     assert lib.fc_attn_fwd(h, 1, 1, 1, 1, 1, 0.0, 0, 1, None, 1, None, 0, None) == -5
     assert lib.fc_attn_bwd(h, *([1] * 8), 0.0, *([1] * 5), None, 0, None) == -5
+    assert lib.fc_attn_bwd_dkdv(h, *([1] * 8), 0.0, *([1] * 4), None, 0, None) == -5
     assert lib.fc_attn_fwd_partial(h, 0, 1, 1, 1, 0.0, 1, 1, None) == -5
     assert lib.fc_lse_merge(1, 1, 1, 1, 4, 2, 96, 1, None, 1, None) == -4
     assert lib.fc_lse_merge(1, 1, 1, 1, -1, 2, 64, 1, None, 1, None) == -1
-    f, b = v.workspace_size(F.FC_TWO_PASS)
+    f, b, k = v.workspace_size(F.FC_TWO_PASS)
     i = v.info
     assert f == 2 * (i["t_q"] * 4 * 64 * 4 + ((i["t_q"] * 4 * 4 + 255) // 256) * 256)
     assert v.workspace_size(F.FC_FUSED)[0] == 0
-    assert lib.fc_workspace_size(h, 7, None, None) == -1
+    assert lib.fc_workspace_size(h, 7, None, None, None) == -1
+    assert k == 0 and b == ((i["t_q"] * 4 * 4 + 255) // 256) * 256   # no split key tile here
     assert lib.fc_view_bind(h, None, 0, None) == -1
     assert lib.fc_view_bind(h, 256, 4, None) == -5       # too small, rejected before any copy
     assert lib.fc_view_bind(h, 257, 1 << 20, None) == -1  # misaligned
@@ -192,3 +194,41 @@ def test_empty_rank_view():
     v = F.View(cu, plan, 2, 1, 4, 4, 64)
     assert v.info["t_q"] == 0 and v.info["t_recv"] == 0 and v.info["n_bwd"] == 0
     v.close()
+
+
+def test_backward_launch_split_covers_the_map():
+    """The backward launch list splits long key tiles into query-range parts
+    (aligned to query tiles) that together cover the canonical item exactly,
+    each split tile with a reduce entry naming consecutive partial slots."""
+    lib = F.lib()
+    for name in ("wholedoc", "llama8b"):
+        w = synth.WORKLOADS[name]
+        cu = synth.cu_seqlens(synth.doc_lengths(name))
+        plan = P.plan_whole_lpt(cu, w.cp) if w.plan == "whole_lpt" else P.plan_per_doc(cu, w.cp)
+        rank = int(np.argmax(P.stats(cu, w.cp, plan, 1, 1)["work"]))
+        v = F.View(cu, plan, w.cp, rank, w.hq, w.hkv, w.d)
+        i = v.info
+        view = V.rank_view(cu, plan, rank)
+        canon = V.bwd_items(view, i["bm_bwd"], i["bn_bwd"])
+        # rebuild the launch list through the device table layout is internal; check via sizes
+        # and by re-deriving the split from the documented rule
+        G = w.hq // w.hkv
+        nt = (canon[:, 3] - canon[:, 2] + i["bm_bwd"] - 1) // i["bm_bwd"]
+        total = int(nt.sum()) * G
+        cap = max(16, -(-total * w.hkv // 512))
+        parts = np.maximum(1, -(-(nt * G) // cap))
+        assert i["n_bwd_reduce"] == int((parts > 1).sum())
+        n_launch = 0
+        slots = 0
+        for n_t, p in zip(nt.tolist(), parts.tolist()):
+            per = -(-n_t // p)
+            k = -(-n_t // per)
+            n_launch += k
+            if p > 1:
+                slots += k
+        assert i["n_bwd_launch"] == n_launch and i["n_bwd_slots"] == slots
+        f, b, k = v.workspace_size()
+        assert k == 2 * slots * w.hkv * 128 * w.d * 4
+        if name == "wholedoc":
+            assert slots > 0
+        v.close()
