@@ -30,11 +30,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(16))) u16 sK[BN * D];
   __shared__ __attribute__((aligned(16))) u16 sQ[2][BM * D];
   __shared__ __attribute__((aligned(16))) u16 sO[2][BM * D];  // dO tiles
-  __shared__ __attribute__((aligned(16))) float sL[2][BM];    // LSE
-  __shared__ __attribute__((aligned(16))) float sD[2][BM];    // delta
-  __shared__ __attribute__((aligned(16))) int sLim[2][BM];
+  __shared__ __attribute__((aligned(16))) float sLD[2][2 * BM];  // LSE, then delta
+  __shared__ __attribute__((aligned(16))) int sLim[2][2 * BM];   // receive limits (first BM)
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5;
   const int b = blockIdx.x;
   const int kvh = b % p.hkv;
@@ -63,9 +62,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   const int ntile = (q1 - q0 + BM - 1) / BM;
   const int n_it = ntile * p.group;
 
-  // next iteration: Q/dO tiles straight into LDS, LSE/D/limit via registers
-  float lpf = 0.f, dpf = 0.f;
-  int mpf = 0;
+  // next iteration: Q/dO tiles, LSE, D and receive limits, all copied from
+  // HBM straight into LDS (rows past q1 repeat the last query; masked)
   const TileLoader<D, BM> ldq(p.hq * D);
   auto fetch = [&](int i_, int buf) {
     const int h = kvh * p.group + i_ / ntile;
@@ -73,19 +71,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
     const size_t base = (size_t(t0) * p.hq + h) * D;
     ldq.load(sQ[buf], p.q + base, q1 - t0);
     ldq.load(sO[buf], p.dout + base, q1 - t0);
-    if (threadIdx.x < BM) {
-      const int qi = min(t0 + int(threadIdx.x), q1 - 1);
-      lpf = p.lse[(size_t)h * p.t_q + qi];
-      dpf = p.delta[(size_t)h * p.t_q + qi];
-      mpf = p.lim[qi];
-    }
-  };
-  auto commit = [&](int buf) {
-    if (threadIdx.x < BM) {
-      sL[buf][threadIdx.x] = lpf;
-      sD[buf][threadIdx.x] = dpf;
-      sLim[buf][threadIdx.x] = mpf;
-    }
+    const int qi = min(t0 + (lane & 31), q1 - 1);
+    if (wave == 0)
+      lds_copy4((half ? p.delta : p.lse) + (size_t)h * p.t_q + qi, sLD[buf]);
+    else if (wave == 1 && src)
+      lds_copy4(p.lim + qi, sLim[buf]);
   };
 
   f32x16 dk[DB], dv[DB];
@@ -98,11 +88,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   const float sl2 = p.scale * kLog2e;
   const int qb = row_base<D>(0, lane), kb = row_base<D>(32 * wave, lane), trb = tr_base<D>(lane);
 
-  if (n_it > 0) {
-    fetch(0, 0);
-    wait_async();
-    commit(0);
-  }
+  if (n_it > 0) fetch(0, 0);
   wait_async();
   __syncthreads();
 
@@ -124,8 +110,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
     const bool edge = diag || !kfull || t0 + BM > q1;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sL[buf][8 * g + 4 * half]);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sD[buf][8 * g + 4 * half]);
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sLD[buf][8 * g + 4 * half]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sLD[buf][BM + 8 * g + 4 * half]);
       int4 m4 = {0, 0, 0, 0};
       if (diag && src) m4 = *reinterpret_cast<const int4*>(&sLim[buf][8 * g + 4 * half]);
       const int lim[4] = {m4.x, m4.y, m4.z, m4.w};
@@ -154,8 +140,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
         dk[db] = mfma32(sa, tread_tr2<D>(Q, trb, 16 * kh, db), dk[db]);
       }
     }
+    __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
     wait_async();
-    if (i_ + 1 < n_it) commit(buf ^ 1);
     __syncthreads();
   }
 

@@ -28,7 +28,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
   __shared__ __attribute__((aligned(16))) u16 sK[2][BN * D];
   __shared__ __attribute__((aligned(16))) u16 sV[2][BN * D];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5;
   const int b = blockIdx.x;
   const int kvh = b % p.hkv;
@@ -120,6 +120,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
       for (int db = 0; db < DB; ++db)
         dq[db] = mfma32(tread_tr2<D>(K, ktb, 16 * kk, db), sb, dq[db]);
     }
+    __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
     wait_async();
     __syncthreads();
   }

@@ -34,7 +34,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   __shared__ __attribute__((aligned(16))) u16 sK[2][BN * D];
   __shared__ __attribute__((aligned(16))) u16 sV[2][BN * D];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5;
   const int b = blockIdx.x;
   const int kvh = b % p.hkv;
@@ -148,6 +148,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       for (int db = 0; db < DB; ++db)
         oacc[db] = mfma32(tread_tr2<D>(V, vtb, 16 * kk, db), pb, oacc[db]);
     }
+    __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
     wait_async();
     __syncthreads();
   }

@@ -169,6 +169,31 @@ __device__ __forceinline__ bf16x8 tread_tr2(const u16* T, int base, int R, int d
   return cat8(a, b);
 }
 
+// One asynchronous 16-byte-per-lane copy from HBM into LDS: lane i's 16 bytes
+// at `g` land at the wave's LDS base `wave_dst` + 16*i. The instruction is
+// issued from inline assembly so that the compiler does not track it: the
+// builtin form makes the compiler wait for every outstanding copy before any
+// later LDS read it cannot prove disjoint, which serialises the double
+// buffering (the read of the current tile would wait for the copy of the
+// next). Completion is the caller's business: wait_async() then a barrier
+// before the destination is read. M0 holds the LDS base; nothing else in
+// these kernels uses M0.
+__device__ __forceinline__ void lds_copy16(const u16* g, u16* wave_dst) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) u16*)wave_dst);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(lds), "v"(g) : "memory");
+}
+
+// The same for 4 bytes per lane: lane i's 4 bytes at `g` land at `wave_dst` +
+// 4*i.
+__device__ __forceinline__ void lds_copy4(const void* g, void* wave_dst) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)wave_dst);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
+               :: "s"(lds), "v"(g) : "memory");
+}
+
 // Asynchronous copies of ROWS x D bf16 tiles (rows row_stride elements apart
 // in HBM) into a swizzled LDS tile, 256 threads. Each thread's chunk offsets
 // are computed once; a load is then one base address plus those offsets.
@@ -200,13 +225,16 @@ struct TileLoader {
         const int r = L / CH;
         if (r >= nvalid) o = (nvalid - 1) * row_stride + 8 * ((L % CH) ^ swz<D>(r));
       }
-      u16* dst = T + (u * 256 + (threadIdx.x & ~63)) * 8;  // wave-uniform base
-      __builtin_amdgcn_global_load_lds(g + o, (__attribute__((address_space(3))) void*)dst, 16,
-                                       0, 0);
+      lds_copy16(g + o, T + (u * 256 + (threadIdx.x & ~63)) * 8);
     }
   }
 };
 
-__device__ __forceinline__ void wait_async() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until every outstanding vector memory load of this wave, the LDS
+// copies included, has completed (s_waitcnt vmcnt(0); the expcnt and
+// lgkmcnt fields are left at their no-wait maxima). Issued through the
+// builtin so that the compiler knows its own earlier loads are complete too
+// and does not add waits of its own inside the loops.
+__device__ __forceinline__ void wait_async() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 }  // namespace fck
