@@ -19,6 +19,8 @@
 #include "common.hpp"
 #include "launch.hpp"
 
+#include <type_traits>
+
 namespace fck {
 
 template <int D>
@@ -27,13 +29,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   constexpr int BM = 32;        // queries per iteration
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
-  __shared__ __attribute__((aligned(16))) u16 sK[BN * D];
-  __shared__ __attribute__((aligned(16))) u16 sQ[2][BM * D];
-  __shared__ __attribute__((aligned(16))) u16 sO[2][BM * D];  // dO tiles
-  __shared__ __attribute__((aligned(16))) float sLD[2][2 * BM];  // LSE, then delta
-  __shared__ __attribute__((aligned(16))) int sLim[2][2 * BM];   // receive limits (first BM)
+  constexpr uint32_t KT = BN * D * 2;  // bytes of the key tile
+  constexpr uint32_t QT = BM * D * 2;  // bytes of a Q or dO tile
+  // LDS layout (bytes): per buffer b, LSE at 256*3b, delta at +256, receive
+  // limits at +512 (a wave-wide copy each, the first BM entries used); then
+  // the key tile; then Q and dO of buffer 0 and of buffer 1. The loop is
+  // unrolled by two, so every read names its buffer with a compile-time
+  // offset (all below 64 KiB, the reach of the offset field).
+  constexpr uint32_t OK = 6 * 256;
+  constexpr uint32_t OQ0 = OK + KT, OO0 = OQ0 + QT, OQ1 = OO0 + QT, OO1 = OQ1 + QT;
+  __shared__ __attribute__((aligned(16))) char smem[OO1 + QT];
 
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5;
   const int b = blockIdx.x;
   const int kvh = b % p.hkv;
@@ -46,9 +53,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   const size_t kvs = size_t(p.hkv) * D, kvo = size_t(kvh) * D;
 
   // key tile (rows past k1 repeat the last key; they are masked)
-  TileLoader<D, BN>(p.hkv * D).load(sK, Kg + size_t(k0) * kvs + kvo, k1 - k0);
-  const int krow = 32 * wave + (lane & 31);  // this lane's key within the tile
-  const int kidx = k0 + krow;
+  TileLoader<D, BN>(p.hkv * D).load_at(lds_addr(smem) + OK, Kg + size_t(k0) * kvs + kvo, k1 - k0);
+  const int kidx = k0 + 32 * wave + (lane & 31);  // this lane's key
   const bool kvalid = kidx < k1;
   // V rows of this lane's key as the B operand of dP = dO V^T
   bf16x8 vreg[KS];
@@ -69,14 +75,25 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
     const int h = kvh * p.group + i_ / ntile;
     const int t0 = q0 + (i_ % ntile) * BM;
     const size_t base = (size_t(t0) * p.hq + h) * D;
-    ldq.load(sQ[buf], p.q + base, q1 - t0);
-    ldq.load(sO[buf], p.dout + base, q1 - t0);
-    const int qi = min(t0 + (lane & 31), q1 - 1);
+    const uint32_t sb = lds_addr(smem);
+    ldq.load_at(sb + (buf ? OQ1 : OQ0), p.q + base, q1 - t0);
+    ldq.load_at(sb + (buf ? OO1 : OO0), p.dout + base, q1 - t0);
+    const uint32_t qoff = 4u * uint32_t(min(t0 + (lane & 31), q1 - 1));
+    const uint32_t sm = sb + 768u * buf;
     if (wave == 0)
-      lds_copy4((half ? p.delta : p.lse) + (size_t)h * p.t_q + qi, sLD[buf]);
-    else if (wave == 1 && src)
-      lds_copy4(p.lim + qi, sLim[buf]);
+      lds_copy4(p.lse + (size_t)h * p.t_q, qoff, sm);
+    else if (wave == 1)
+      lds_copy4(p.delta + (size_t)h * p.t_q, qoff, sm + 256);
+    else if (wave == 2 && src)
+      lds_copy4(p.lim, qoff, sm + 512);
   };
+
+  // per-lane LDS byte offsets (swizzled tiles): row reads of a 32-row block
+  // (Q and dO tiles; the key rows are the same plus this wave's block) and
+  // transpose reads; a k-step or column block is an XOR of a constant
+  uint32_t pr = 2u * uint32_t(row_base<D>(0, lane));
+  uint32_t pt = 2u * uint32_t(tr_base<D>(lane));
+  const uint32_t kofs = OK + uint32_t(wave) * 64u * D;  // this wave's key rows
 
   f32x16 dk[DB], dv[DB];
 #pragma unroll
@@ -86,43 +103,48 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   }
   const bool kfull = k1 - k0 == BN;
   const float sl2 = p.scale * kLog2e;
-  const int qb = row_base<D>(0, lane), kb = row_base<D>(32 * wave, lane), trb = tr_base<D>(lane);
+  // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
+  const int kx = kvalid ? kidx : 0x7fffffff;  // never below a receive limit
 
   if (n_it > 0) fetch(0, 0);
   wait_async();
   __syncthreads();
 
-  for (int i_ = 0; i_ < n_it; ++i_) {
-    const int buf = i_ & 1;
+  auto step = [&](int i_, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    constexpr uint32_t QO = B ? OQ1 : OQ0, OO = B ? OO1 : OO0, SO = 768u * B;
     const int t0 = q0 + (i_ % ntile) * BM;
-    if (i_ + 1 < n_it) fetch(i_ + 1, buf ^ 1);
-    const u16* Q = sQ[buf];
-    const u16* O = sO[buf];
+    if (i_ + 1 < n_it) fetch(i_ + 1, B ^ 1);
+    pr = opaque(pr);
+    pt = opaque(pt);
 
     f32x16 sacc = zero16(), dpacc = zero16();
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      sacc = mfma32(tread8_ks<D>(Q, qb, ks), tread8_ks<D>(sK, kb, ks), sacc);
-      dpacc = mfma32(tread8_ks<D>(O, qb, ks), vreg[ks], dpacc);
+      const uint32_t r = pr ^ (ks << 5);
+      sacc = mfma32(lds_b128(smem, r, QO), lds_b128(smem, r + kofs, 0), sacc);
+      dpacc = mfma32(lds_b128(smem, r, OO), vreg[ks], dpacc);
     }
-    // this lane's 16 query rows are 8g + 4*half + 0..3, g = 0..3
+    // this lane's 16 query rows are t0 + 4*half + 8g + j (register 4g + j)
     const bool diag = t0 < qfull;
     const bool edge = diag || !kfull || t0 + BM > q1;
+    const int hiq = q1 - t0 - 4 * half;  // rows cq < hiq exist
+    // local diagonal: the key is seen by rows cq >= lo; otherwise by all
+    // rows if the key exists
+    const int lo = !kvalid ? 0x40000000 : (diag && !src) ? kidx - t0 - 4 * half : -0x40000000;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sLD[buf][8 * g + 4 * half]);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sLD[buf][BM + 8 * g + 4 * half]);
-      int4 m4 = {0, 0, 0, 0};
-      if (diag && src) m4 = *reinterpret_cast<const int4*>(&sLim[buf][8 * g + 4 * half]);
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(smem + SO + 4 * (8 * g + 4 * half));
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(smem + SO + 256 + 4 * (8 * g + 4 * half));
+      int4 m4 = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+      if (diag && src) m4 = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
       const int lim[4] = {m4.x, m4.y, m4.z, m4.w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int i = 4 * g + j;
+        const int i = 4 * g + j, cq = 8 * g + j;
         float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -l4[j] * kLog2e));
         if (edge) {
-          const int qi = t0 + 8 * g + 4 * half + j;
-          bool vis = kvalid && qi < q1;
-          if (diag) vis = vis && (src ? kidx < lim[j] : kidx <= qi);
+          const bool vis = (cq >= lo) & (cq < hiq) & (kx < lim[j]);
           pij = vis ? pij : 0.f;
         }
         sacc[i] = pij;
@@ -136,13 +158,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
       const bf16x8 sa = pack8(dpacc, 8 * kh);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        dv[db] = mfma32(pa, tread_tr2<D>(O, trb, 16 * kh, db), dv[db]);
-        dk[db] = mfma32(sa, tread_tr2<D>(Q, trb, 16 * kh, db), dk[db]);
+        const uint32_t t0_ = pt ^ (db << 6), t1_ = (pt ^ ((db << 6) | 32)) + 16 * D;
+        dv[db] = mfma32(pa, cat8(lds_tr(smem, t0_, OO + kh * 32 * D),
+                                 lds_tr(smem, t1_, OO + kh * 32 * D)), dv[db]);
+        dk[db] = mfma32(sa, cat8(lds_tr(smem, t0_, QO + kh * 32 * D),
+                                 lds_tr(smem, t1_, QO + kh * 32 * D)), dk[db]);
       }
     }
     __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
     wait_async();
     __syncthreads();
+  };
+  for (int i_ = 0; i_ < n_it; i_ += 2) {
+    step(i_, std::integral_constant<int, 0>());
+    if (i_ + 1 < n_it) step(i_ + 1, std::integral_constant<int, 1>());
   }
 
   // dK/dV of this tile, or of this part of a split tile (partial slot)

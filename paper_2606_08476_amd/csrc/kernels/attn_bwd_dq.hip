@@ -17,6 +17,8 @@
 #include "common.hpp"
 #include "launch.hpp"
 
+#include <type_traits>
+
 namespace fck {
 
 template <int D, int HPW>
@@ -25,10 +27,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
   constexpr int WPH = 4 / HPW;
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
-  __shared__ __attribute__((aligned(16))) u16 sK[2][BN * D];
-  __shared__ __attribute__((aligned(16))) u16 sV[2][BN * D];
+  constexpr uint32_t TILE = BN * D * 2;  // bytes of one K or V tile
+  // LDS: K0 | V0 | K1 | V1 (double buffer); the loop is unrolled by two so
+  // every read names its buffer with a compile-time offset
+  __shared__ __attribute__((aligned(16))) char smem[4 * TILE];
 
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5;
   const int b = blockIdx.x;
   const int kvh = b % p.hkv;
@@ -47,13 +51,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
   const int n_t = n_r + (l1 - l0 + BN - 1) / BN;
 
   const TileLoader<D, BN> ld(p.hkv * D);
-  auto fetch = [&](int j, int buf) {
+  auto fetch = [&](int j, uint32_t kofs) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
     const size_t base = (size_t(k0) * p.hkv + kvh) * D;
-    ld.load(sK[buf], (rs ? p.k_recv : p.k_loc) + base, hi - k0);
-    ld.load(sV[buf], (rs ? p.v_recv : p.v_loc) + base, hi - k0);
+    ld.load_at(lds_addr(smem) + kofs, (rs ? p.k_recv : p.k_loc) + base, hi - k0);
+    ld.load_at(lds_addr(smem) + kofs + TILE, (rs ? p.v_recv : p.v_loc) + base, hi - k0);
   };
 
   if (n_t > 0) fetch(0, 0);
@@ -73,43 +77,60 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
     }
   }
 
-  const int kb0 = row_base<D>(0, lane), kb1 = row_base<D>(32, lane), ktb = tr_base<D>(lane);
+  // per-lane LDS byte offsets: K/V rows for k-step ks, and the two transpose
+  // reads of K^T block db
+  uint32_t pr[KS], pt[DB][2];
+  {
+    const int rb = row_base<D>(0, lane), tb = tr_base<D>(lane);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) pr[ks] = 2u * uint32_t(rb ^ (ks << 4));
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      pt[db][0] = 2u * uint32_t(tb ^ (db << 5));
+      pt[db][1] = 2u * uint32_t((tb ^ ((db << 5) | 16)) + 8 * D);
+    }
+  }
+
   f32x16 dq[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
   wait_async();
   __syncthreads();
 
-  for (int j = 0; j < n_t; ++j) {
-    const int buf = j & 1;
-    if (j + 1 < n_t) fetch(j + 1, buf ^ 1);
+  auto step = [&](int j, auto buf) {
+    constexpr uint32_t KO = decltype(buf)::value * 2 * TILE, VO = KO + TILE;
+    if (j + 1 < n_t) fetch(j + 1, 2 * TILE - KO);
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
-    const u16* K = sK[buf];
-    const u16* V = sV[buf];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) pr[ks] = opaque(pr[ks]);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      pt[db][0] = opaque(pt[db][0]);
+      pt[db][1] = opaque(pt[db][1]);
+    }
 
-    // four independent accumulator chains, interleaved
+    // S^T = K Q^T and dP^T = V dO^T, four independent accumulator chains
     f32x16 s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) {
-        s[mb] = mfma32(tread8_ks<D>(K, mb ? kb1 : kb0, ks), qreg[ks], s[mb]);
-        dp[mb] = mfma32(tread8_ks<D>(V, mb ? kb1 : kb0, ks), oreg[ks], dp[mb]);
+        s[mb] = mfma32(lds_b128(smem, pr[ks], KO + mb * 64 * D), qreg[ks], s[mb]);
+        dp[mb] = mfma32(lds_b128(smem, pr[ks], VO + mb * 64 * D), oreg[ks], dp[mb]);
       }
+    // P = exp(S - LSE), dS = P (dP - D); masked scores (keys past the range,
+    // later keys on diagonal tiles) give P = 0
     const bool diag = !rs && k0 >= ldiag;
     const bool edge = diag || k0 + BN > hi;
+    const int rel = (diag ? min(hi, qrow + 1) : hi) - k0 - 4 * half;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], sl2, -lse2));
-        if (edge) {
-          const int kr = k0 + mb * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
-          const bool vis = kr < hi && (!diag || kr <= qrow);
-          pij = vis ? pij : 0.f;
-        }
+        if (edge) pij = mb * 32 + 8 * (i >> 2) + (i & 3) < rel ? pij : 0.f;
         dp[mb][i] = pij * (dp[mb][i] - del);
       }
     // dQ^T += K^T dS^T, 16 keys per MFMA step
@@ -117,12 +138,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
     for (int kk = 0; kk < 4; ++kk) {
       const bf16x8 sb = pack8(dp[kk >> 1], 8 * (kk & 1));
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
-        dq[db] = mfma32(tread_tr2<D>(K, ktb, 16 * kk, db), sb, dq[db]);
+      for (int db = 0; db < DB; ++db) {
+        const uint32_t ro = KO + kk * 32 * D;
+        dq[db] = mfma32(cat8(lds_tr(smem, pt[db][0], ro), lds_tr(smem, pt[db][1], ro)), sb, dq[db]);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
     wait_async();
     __syncthreads();
+  };
+  for (int j = 0; j < n_t; j += 2) {
+    step(j, std::integral_constant<int, 0>());
+    if (j + 1 < n_t) step(j + 1, std::integral_constant<int, 1>());
   }
 
   if (qvalid) {

@@ -22,6 +22,8 @@
 #include "common.hpp"
 #include "launch.hpp"
 
+#include <type_traits>
+
 namespace fck {
 
 template <int D, int HPW, bool FINAL>
@@ -31,10 +33,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   constexpr int KS = D / 16;    // MFMA k-steps over the head dim
   constexpr int DB = D / 32;    // 32-wide output blocks of the head dim
   constexpr float kLazy = 8.0f; // log2 headroom before rescaling
-  __shared__ __attribute__((aligned(16))) u16 sK[2][BN * D];
-  __shared__ __attribute__((aligned(16))) u16 sV[2][BN * D];
+  constexpr uint32_t TILE = BN * D * 2;  // bytes of one K or V tile
+  // LDS: K0 | V0 | K1 | V1 (double buffer). The loop is unrolled by two, so
+  // every read names its buffer with a compile-time offset.
+  __shared__ __attribute__((aligned(16))) char smem[4 * TILE];
 
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5;
   const int b = blockIdx.x;
   const int kvh = b % p.hkv;
@@ -53,16 +57,17 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int n_r = (r1 - r0 + BN - 1) / BN;
   const int n_t = n_r + (l1 - l0 + BN - 1) / BN;
 
-  // async load of key tile j into buffer `buf`; rows past the range repeat
-  // the last row (finite data; those keys are masked)
+  // async copy of key tile j into the buffer at byte offset `kofs` (K, then
+  // V at +TILE); rows past the range repeat the last row (finite data; those
+  // keys are masked)
   const TileLoader<D, BN> ld(p.hkv * D);
-  auto fetch = [&](int j, int buf) {
+  auto fetch = [&](int j, uint32_t kofs) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
     const size_t base = (size_t(k0) * p.hkv + kvh) * D;
-    ld.load(sK[buf], (rs ? p.k_recv : p.k_loc) + base, hi - k0);
-    ld.load(sV[buf], (rs ? p.v_recv : p.v_loc) + base, hi - k0);
+    ld.load_at(lds_addr(smem) + kofs, (rs ? p.k_recv : p.k_loc) + base, hi - k0);
+    ld.load_at(lds_addr(smem) + kofs + TILE, (rs ? p.v_recv : p.v_loc) + base, hi - k0);
   };
 
   if (n_t > 0) fetch(0, 0);
@@ -75,7 +80,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       qreg[ks] = qvalid ? *reinterpret_cast<const bf16x8*>(qp + 16 * ks) : zero8();
   }
 
-  const int kb0 = row_base<D>(0, lane), kb1 = row_base<D>(32, lane), vtb = tr_base<D>(lane);
+  // per-lane LDS byte offsets of the MFMA operand reads (swizzled tiles):
+  // K rows for k-step ks, and the two transpose reads of V^T block db
+  uint32_t pk[KS], pv[DB][2];
+  {
+    const int kb = row_base<D>(0, lane), vb = tr_base<D>(lane);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) pk[ks] = 2u * uint32_t(kb ^ (ks << 4));
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      pv[db][0] = 2u * uint32_t(vb ^ (db << 5));
+      pv[db][1] = 2u * uint32_t((vb ^ ((db << 5) | 16)) + 8 * D);
+    }
+  }
+
   f32x16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) oacc[db] = zero16();
@@ -84,33 +102,38 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   wait_async();
   __syncthreads();
 
-  for (int j = 0; j < n_t; ++j) {
-    const int buf = j & 1;
-    if (j + 1 < n_t) fetch(j + 1, buf ^ 1);
+  auto step = [&](int j, auto buf) {
+    constexpr uint32_t KO = decltype(buf)::value * 2 * TILE, VO = KO + TILE;
+    if (j + 1 < n_t) fetch(j + 1, 2 * TILE - KO);
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
-    const u16* K = sK[buf];
-    const u16* V = sV[buf];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) pk[ks] = opaque(pk[ks]);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      pv[db][0] = opaque(pv[db][0]);
+      pv[db][1] = opaque(pv[db][1]);
+    }
 
-    // two independent accumulator chains, interleaved
+    // S^T = K Q^T, two independent accumulator chains (32 keys each)
     f32x16 s[2] = {zero16(), zero16()};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
-        s[mb] = mfma32(tread8_ks<D>(K, mb ? kb1 : kb0, ks), qreg[ks], s[mb]);
-    // mask keys past the range and, on diagonal tiles, keys after the query
+        s[mb] = mfma32(lds_b128(smem, pk[ks], KO + mb * 64 * D), qreg[ks], s[mb]);
+    // mask keys past the range and, on diagonal tiles, keys after the query:
+    // element i of block mb is key k0 + 4*half + cst(mb, i), visible iff
+    // cst < rel (one compare per score)
     const bool diag = !rs && k0 >= ldiag;
     if (diag || k0 + BN > hi) {
+      const int rel = (diag ? min(hi, qrow + 1) : hi) - k0 - 4 * half;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int kr = k0 + mb * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
-          const bool vis = kr < hi && (!diag || kr <= qrow);
-          s[mb][i] = vis ? s[mb][i] : -INFINITY;
-        }
+        for (int i = 0; i < 16; ++i)
+          s[mb][i] = mb * 32 + 8 * (i >> 2) + (i & 3) < rel ? s[mb][i] : -INFINITY;
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -145,12 +168,19 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     for (int kk = 0; kk < 4; ++kk) {
       const bf16x8 pb = pack8(s[kk >> 1], 8 * (kk & 1));
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
-        oacc[db] = mfma32(tread_tr2<D>(V, vtb, 16 * kk, db), pb, oacc[db]);
+      for (int db = 0; db < DB; ++db) {
+        const uint32_t ro = VO + kk * 32 * D;  // rows 16*kk..
+        oacc[db] = mfma32(cat8(lds_tr(smem, pv[db][0], ro), lds_tr(smem, pv[db][1], ro)), pb,
+                          oacc[db]);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
     wait_async();
     __syncthreads();
+  };
+  for (int j = 0; j < n_t; j += 2) {
+    step(j, std::integral_constant<int, 0>());
+    if (j + 1 < n_t) step(j + 1, std::integral_constant<int, 1>());
   }
 
   lsum += __shfl_xor(lsum, 32);

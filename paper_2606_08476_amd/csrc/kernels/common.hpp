@@ -169,42 +169,66 @@ __device__ __forceinline__ bf16x8 tread_tr2(const u16* T, int base, int R, int d
   return cat8(a, b);
 }
 
-// One asynchronous 16-byte-per-lane copy from HBM into LDS: lane i's 16 bytes
-// at `g` land at the wave's LDS base `wave_dst` + 16*i. The instruction is
-// issued from inline assembly so that the compiler does not track it: the
-// builtin form makes the compiler wait for every outstanding copy before any
-// later LDS read it cannot prove disjoint, which serialises the double
-// buffering (the read of the current tile would wait for the copy of the
-// next). Completion is the caller's business: wait_async() then a barrier
-// before the destination is read. M0 holds the LDS base; nothing else in
-// these kernels uses M0.
-__device__ __forceinline__ void lds_copy16(const u16* g, u16* wave_dst) {
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) u16*)wave_dst);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :: "s"(lds), "v"(g) : "memory");
+// LDS reads at byte addresses: `smem` is a kernel's shared array, `v` a
+// per-lane byte offset in a register and `imm` a compile-time byte offset
+// (buffer, row block), which the compiler folds into the instruction's
+// offset field.
+__device__ __forceinline__ bf16x8 lds_b128(const void* smem, uint32_t v, uint32_t imm) {
+  return *reinterpret_cast<const bf16x8*>(static_cast<const char*>(smem) + v + imm);
+}
+__device__ __forceinline__ bf16x4 lds_tr(const void* smem, uint32_t v, uint32_t imm) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4*)((__attribute__((address_space(3))) char*)smem + v + imm));
 }
 
-// The same for 4 bytes per lane: lane i's 4 bytes at `g` land at `wave_dst` +
-// 4*i.
-__device__ __forceinline__ void lds_copy4(const void* g, void* wave_dst) {
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)wave_dst);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
-               :: "s"(lds), "v"(g) : "memory");
+// A copy of `x` the compiler cannot see through. Taken once per loop
+// iteration of a per-lane address, it keeps `x + constant` inside the loop,
+// so the constant lands in the LDS instruction's offset field instead of a
+// register of its own per distinct constant.
+__device__ __forceinline__ uint32_t opaque(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// Asynchronous HBM-to-LDS copies. Lane i's 16 (or 4) bytes at `gbase` +
+// `voff` land at LDS byte address `lds` + 16*i (4*i); `gbase` and `lds` are
+// wave-uniform. The instruction is issued from inline assembly so that the
+// compiler does not track it: with the builtin form the compiler waits for
+// every outstanding copy before any later LDS read it cannot prove disjoint,
+// which serialises the double buffering (reads of the current tile would
+// wait for the copy of the next). Completion is the caller's business:
+// wait_async() then a barrier before the destination is read. M0 holds the
+// LDS address; nothing else in these kernels uses M0.
+__device__ __forceinline__ void lds_copy16(const void* gbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(lds), "v"(voff), "s"(gbase) : "memory");
+}
+__device__ __forceinline__ void lds_copy4(const void* gbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2"
+               :: "s"(lds), "v"(voff), "s"(gbase) : "memory");
+}
+
+// LDS byte address of a pointer into shared memory.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// Index of this thread's wave in the workgroup, as a wave-uniform value.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
 
 // Asynchronous copies of ROWS x D bf16 tiles (rows row_stride elements apart
-// in HBM) into a swizzled LDS tile, 256 threads. Each thread's chunk offsets
-// are computed once; a load is then one base address plus those offsets.
-// Rows at or past `nvalid` repeat row nvalid-1 (finite data for masked
-// rows, no read past the range). Completion: wait_async() then a barrier.
+// in HBM) into a swizzled LDS tile, 256 threads. Each thread's chunk byte
+// offsets are computed once; a copy is then one uniform base address plus
+// those offsets. Rows at or past `nvalid` repeat row nvalid-1 (finite data
+// for masked rows, no read past the range).
 template <int D, int ROWS>
 struct TileLoader {
   static constexpr int CH = D / 8;
   static constexpr int N = ROWS * CH / 256;
   static_assert((ROWS * CH) % 256 == 0, "tile must be a multiple of 256 chunks");
-  int off[N];
+  uint32_t off[N];
   int row_stride;
 
   __device__ __forceinline__ explicit TileLoader(int stride) : row_stride(stride) {
@@ -212,20 +236,25 @@ struct TileLoader {
     for (int u = 0; u < N; ++u) {
       const int L = u * 256 + threadIdx.x;
       const int r = L / CH;
-      off[u] = r * stride + 8 * ((L % CH) ^ swz<D>(r));
+      off[u] = 2u * uint32_t(r * stride + 8 * ((L % CH) ^ swz<D>(r)));
     }
   }
 
   __device__ __forceinline__ void load(u16* T, const u16* g, int nvalid) const {
+    load_at(lds_addr(T), g, nvalid);
+  }
+  // the same with the tile's LDS byte address
+  __device__ __forceinline__ void load_at(uint32_t tile, const u16* g, int nvalid) const {
+    const uint32_t lds = tile + 1024u * wave_id();
 #pragma unroll
     for (int u = 0; u < N; ++u) {
-      int o = off[u];
+      uint32_t o = off[u];
       if (nvalid < ROWS) {  // uniform: only the last, ragged tile of a range
         const int L = u * 256 + threadIdx.x;
         const int r = L / CH;
-        if (r >= nvalid) o = (nvalid - 1) * row_stride + 8 * ((L % CH) ^ swz<D>(r));
+        if (r >= nvalid) o = 2u * uint32_t((nvalid - 1) * row_stride + 8 * ((L % CH) ^ swz<D>(r)));
       }
-      lds_copy16(g + o, T + (u * 256 + (threadIdx.x & ~63)) * 8);
+      lds_copy16(g, o, lds + 4096u * u);
     }
   }
 };
