@@ -110,6 +110,16 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
   wait_async();
   __syncthreads();
 
+  // One query tile. The 4*KS... MFMAs of the step run as one software
+  // pipeline of slots, in this order:
+  //   S = Q K^T (KS slots); dP = dO V^T (KS slots, each also computing part of
+  //   P = exp(S - LSE)); dV += P^T dO (2*DB slots, each also computing part
+  //   of dS = P (dP - D)); dK += dS^T Q (2*DB slots).
+  // Each slot issues the LDS reads of the slot two ahead, its MFMA, and its
+  // share of the vector work, which then runs while the MFMA does; a
+  // scheduling barrier after each slot keeps this order.
+  constexpr int NS = 2 * KS + 4 * DB;       // slots per step
+  constexpr int EP = 16 / KS, ES = 8 / DB;  // P / dS elements per slot
   auto step = [&](int i_, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     constexpr uint32_t QO = B ? OQ1 : OQ0, OO = B ? OO1 : OO0, SO = 768u * B;
@@ -117,55 +127,81 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
     if (i_ + 1 < n_it) fetch(i_ + 1, B ^ 1);
     pr = opaque(pr);
     pt = opaque(pt);
+    // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
+    // (register 4g + j): rows cq < hiq exist; on a local diagonal the key is
+    // seen by rows cq >= lo; on a received diagonal by rows whose receive
+    // limit exceeds the key index
+    const bool diag = t0 < qfull;
+    const int hiq = q1 - t0 - 4 * half;
+    const int lo = !kvalid ? 0x40000000 : (diag && !src) ? kidx - t0 - 4 * half : -0x40000000;
+    const int kl = (diag && src) ? kx : -0x7fffffff;
 
     f32x16 sacc = zero16(), dpacc = zero16();
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const uint32_t r = pr ^ (ks << 5);
-      sacc = mfma32(lds_b128(smem, r, QO), lds_b128(smem, r + kofs, 0), sacc);
-      dpacc = mfma32(lds_b128(smem, r, OO), vreg[ks], dpacc);
-    }
-    // this lane's 16 query rows are t0 + 4*half + 8g + j (register 4g + j)
-    const bool diag = t0 < qfull;
-    const bool edge = diag || !kfull || t0 + BM > q1;
-    const int hiq = q1 - t0 - 4 * half;  // rows cq < hiq exist
-    // local diagonal: the key is seen by rows cq >= lo; otherwise by all
-    // rows if the key exists
-    const int lo = !kvalid ? 0x40000000 : (diag && !src) ? kidx - t0 - 4 * half : -0x40000000;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(smem + SO + 4 * (8 * g + 4 * half));
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(smem + SO + 256 + 4 * (8 * g + 4 * half));
-      int4 m4 = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
-      if (diag && src) m4 = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
-      const int lim[4] = {m4.x, m4.y, m4.z, m4.w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int i = 4 * g + j, cq = 8 * g + j;
-        float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[i], sl2, -l4[j] * kLog2e));
-        if (edge) {
-          const bool vis = (cq >= lo) & (cq < hiq) & (kx < lim[j]);
-          pij = vis ? pij : 0.f;
-        }
-        sacc[i] = pij;
-        dpacc[i] = pij * (dpacc[i] - d4[j]);
-      }
-    }
-    // dV += P^T dO and dK += dS^T Q (scale applied at the end)
-#pragma unroll
-    for (int kh = 0; kh < 2; ++kh) {
-      const bf16x8 pa = pack8(sacc, 8 * kh);
-      const bf16x8 sa = pack8(dpacc, 8 * kh);
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
+    bf16x8 ra[3], rb[3], pa[2], sa[2];
+    f32x4 l4[4], d4[4];
+    int4 m4[4];
+    // LDS operand reads of slot n into ring entry n % 3
+    auto rd = [&](int n) {
+      bf16x8& a = ra[n % 3];
+      if (n < KS) {
+        const uint32_t r = pr ^ (n << 5);
+        a = lds_b128(smem, r, QO);
+        rb[n % 3] = lds_b128(smem, r + kofs, 0);
+      } else if (n < 2 * KS) {
+        a = lds_b128(smem, pr ^ ((n - KS) << 5), OO);
+      } else {
+        const int u = n < 2 * KS + 2 * DB ? n - 2 * KS : n - 2 * KS - 2 * DB;
+        const int kh = u / DB, db = u % DB;
+        const uint32_t base = (n < 2 * KS + 2 * DB ? OO : QO) + kh * 32 * D;
         const uint32_t t0_ = pt ^ (db << 6), t1_ = (pt ^ ((db << 6) | 32)) + 16 * D;
-        dv[db] = mfma32(pa, cat8(lds_tr(smem, t0_, OO + kh * 32 * D),
-                                 lds_tr(smem, t1_, OO + kh * 32 * D)), dv[db]);
-        dk[db] = mfma32(sa, cat8(lds_tr(smem, t0_, QO + kh * 32 * D),
-                                 lds_tr(smem, t1_, QO + kh * 32 * D)), dk[db]);
+        a = cat8(lds_tr(smem, t0_, base), lds_tr(smem, t1_, base));
       }
+    };
+    rd(0);
+    rd(1);
+#pragma unroll
+    for (int n = 0; n < NS; ++n) {
+      if (n + 2 < NS) rd(n + 2);
+      if (n == KS - 2) {  // LSE, delta and limits of the 16 rows
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          l4[g] = *reinterpret_cast<const f32x4*>(smem + SO + 4 * (8 * g + 4 * half));
+          m4[g] = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
+        }
+      }
+      if (n == KS - 1) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          d4[g] = *reinterpret_cast<const f32x4*>(smem + SO + 256 + 4 * (8 * g + 4 * half));
+      }
+      const bf16x8& a = ra[n % 3];
+      if (n < KS) {
+        sacc = mfma32(a, rb[n % 3], sacc);
+      } else if (n < 2 * KS) {
+        dpacc = mfma32(a, vreg[n - KS], dpacc);
+#pragma unroll
+        for (int e = (n - KS) * EP; e < (n - KS + 1) * EP; ++e) {
+          const int g = e >> 2, j = e & 3, cq = 8 * g + j;
+          const int lim = j == 0 ? m4[g].x : j == 1 ? m4[g].y : j == 2 ? m4[g].z : m4[g].w;
+          const float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], sl2, -l4[g][j] * kLog2e));
+          sacc[e] = ((cq >= lo) & (cq < hiq) & (kl < lim)) ? pij : 0.f;
+        }
+        if ((n - KS + 1) * EP == 8) pa[0] = pack8(sacc, 0);
+        if ((n - KS + 1) * EP == 16) pa[1] = pack8(sacc, 8);
+      } else if (n < 2 * KS + 2 * DB) {
+        const int u = n - 2 * KS, kh = u / DB, db = u % DB;
+        dv[db] = mfma32(pa[kh], a, dv[db]);
+#pragma unroll
+        for (int e = u * ES; e < (u + 1) * ES; ++e)
+          dpacc[e] = sacc[e] * (dpacc[e] - d4[e >> 2][e & 3]);
+        if ((u + 1) * ES == 8) sa[0] = pack8(dpacc, 0);
+        if ((u + 1) * ES == 16) sa[1] = pack8(dpacc, 8);
+      } else {
+        const int u = n - 2 * KS - 2 * DB, kh = u / DB, db = u % DB;
+        dk[db] = mfma32(sa[kh], a, dk[db]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
     wait_async();
     __syncthreads();
   };

@@ -219,22 +219,22 @@ __device__ __forceinline__ int wave_id() {
 }
 
 // Asynchronous copies of ROWS x D bf16 tiles (rows row_stride elements apart
-// in HBM) into a swizzled LDS tile, 256 threads. Each thread's chunk byte
-// offsets are computed once; a copy is then one uniform base address plus
-// those offsets. Rows at or past `nvalid` repeat row nvalid-1 (finite data
-// for masked rows, no read past the range).
-template <int D, int ROWS>
+// in HBM) into a swizzled LDS tile by a workgroup of NT threads. Each
+// thread's chunk byte offsets are computed once; a copy is then one uniform
+// base address plus those offsets. Rows at or past `nvalid` repeat row
+// nvalid-1 (finite data for masked rows, no read past the range).
+template <int D, int ROWS, int NT = 256>
 struct TileLoader {
   static constexpr int CH = D / 8;
-  static constexpr int N = ROWS * CH / 256;
-  static_assert((ROWS * CH) % 256 == 0, "tile must be a multiple of 256 chunks");
+  static constexpr int N = ROWS * CH / NT;
+  static_assert((ROWS * CH) % NT == 0, "tile must be a multiple of NT chunks");
   uint32_t off[N];
   int row_stride;
 
   __device__ __forceinline__ explicit TileLoader(int stride) : row_stride(stride) {
 #pragma unroll
     for (int u = 0; u < N; ++u) {
-      const int L = u * 256 + threadIdx.x;
+      const int L = u * NT + threadIdx.x;
       const int r = L / CH;
       off[u] = 2u * uint32_t(r * stride + 8 * ((L % CH) ^ swz<D>(r)));
     }
@@ -250,11 +250,11 @@ struct TileLoader {
     for (int u = 0; u < N; ++u) {
       uint32_t o = off[u];
       if (nvalid < ROWS) {  // uniform: only the last, ragged tile of a range
-        const int L = u * 256 + threadIdx.x;
+        const int L = u * NT + threadIdx.x;
         const int r = L / CH;
         if (r >= nvalid) o = 2u * uint32_t((nvalid - 1) * row_stride + 8 * ((L % CH) ^ swz<D>(r)));
       }
-      lds_copy16(g, o, lds + 4096u * u);
+      lds_copy16(g, o, lds + 16u * NT * u);
     }
   }
 };
