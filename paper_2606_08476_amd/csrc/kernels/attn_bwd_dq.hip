@@ -97,6 +97,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
   wait_async();
   __syncthreads();
 
+  // One key tile. Its MFMAs run as one software pipeline of slots:
+  //   S^T, keys 0-31; S^T, keys 32-63 (with P of keys 0-31); dP^T, keys 0-31
+  //   (with P of keys 32-63); dP^T, keys 32-63 (with dS of keys 0-31);
+  //   dQ^T += K^T dS^T over keys 0-31 (with dS of keys 32-63), then 32-63.
+  // Each slot issues the LDS reads of the slot two ahead, its MFMA and its
+  // share of the vector work, which runs while the MFMA does; a scheduling
+  // barrier after each slot keeps this order.
+  constexpr int NS = 4 * KS + 4 * DB;        // slots per tile
+  constexpr int EP = 16 / KS, EQ = 8 / DB;   // elements per slot (P, dS)
   auto step = [&](int j, auto buf) {
     constexpr uint32_t KO = decltype(buf)::value * 2 * TILE, VO = KO + TILE;
     if (j + 1 < n_t) fetch(j + 1, 2 * TILE - KO);
@@ -110,40 +119,66 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(DqParams p) {
       pt[db][0] = opaque(pt[db][0]);
       pt[db][1] = opaque(pt[db][1]);
     }
-
-    // S^T = K Q^T and dP^T = V dO^T, four independent accumulator chains
-    f32x16 s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        s[mb] = mfma32(lds_b128(smem, pr[ks], KO + mb * 64 * D), qreg[ks], s[mb]);
-        dp[mb] = mfma32(lds_b128(smem, pr[ks], VO + mb * 64 * D), oreg[ks], dp[mb]);
-      }
-    // P = exp(S - LSE), dS = P (dP - D); masked scores (keys past the range,
-    // later keys on diagonal tiles) give P = 0
+    // key k0 + 4*half + c (c = 32*mb + 8*(i/4) + i%4 for register i) is seen
+    // iff c < rel: keys past the range, and later keys on diagonal tiles,
+    // give P = 0
     const bool diag = !rs && k0 >= ldiag;
-    const bool edge = diag || k0 + BN > hi;
     const int rel = (diag ? min(hi, qrow + 1) : hi) - k0 - 4 * half;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], sl2, -lse2));
-        if (edge) pij = mb * 32 + 8 * (i >> 2) + (i & 3) < rel ? pij : 0.f;
-        dp[mb][i] = pij * (dp[mb][i] - del);
-      }
-    // dQ^T += K^T dS^T, 16 keys per MFMA step
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const bf16x8 sb = pack8(dp[kk >> 1], 8 * (kk & 1));
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
+
+    f32x16 s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
+    bf16x8 ring[3], sb[4];
+    auto rd = [&](int n) {
+      bf16x8& a = ring[n % 3];
+      if (n < 4 * KS) {  // K rows (S) or V rows (dP)
+        const int ks = n % KS, mb = (n / KS) & 1;
+        a = lds_b128(smem, pr[ks], (n < 2 * KS ? KO : VO) + mb * 64 * D);
+      } else {  // K^T for dQ
+        const int u = n - 4 * KS, kk = u / DB, db = u % DB;
         const uint32_t ro = KO + kk * 32 * D;
-        dq[db] = mfma32(cat8(lds_tr(smem, pt[db][0], ro), lds_tr(smem, pt[db][1], ro)), sb, dq[db]);
+        a = cat8(lds_tr(smem, pt[db][0], ro), lds_tr(smem, pt[db][1], ro));
       }
+    };
+    auto pexp = [&](int mb, int i) {
+      const float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], sl2, -lse2));
+      s[mb][i] = 32 * mb + 8 * (i >> 2) + (i & 3) < rel ? pij : 0.f;
+    };
+    auto dsv = [&](int mb, int i) { dp[mb][i] = s[mb][i] * (dp[mb][i] - del); };
+    rd(0);
+    rd(1);
+#pragma unroll
+    for (int n = 0; n < NS; ++n) {
+      if (n + 2 < NS) rd(n + 2);
+      const bf16x8& a = ring[n % 3];
+      if (n < 2 * KS) {
+        const int ks = n % KS, mb = n / KS;
+        s[mb] = mfma32(a, qreg[ks], s[mb]);
+        if (mb == 1)
+#pragma unroll
+          for (int e = ks * EP; e < (ks + 1) * EP; ++e) pexp(0, e);
+      } else if (n < 4 * KS) {
+        const int ks = n % KS, mb = (n - 2 * KS) / KS;
+        dp[mb] = mfma32(a, oreg[ks], dp[mb]);
+        if (mb == 0) {
+#pragma unroll
+          for (int e = ks * EP; e < (ks + 1) * EP; ++e) pexp(1, e);
+        } else {
+#pragma unroll
+          for (int e = ks * EP; e < (ks + 1) * EP; ++e) dsv(0, e);
+          if ((ks + 1) * EP == 8) sb[0] = pack8(dp[0], 0);
+          if ((ks + 1) * EP == 16) sb[1] = pack8(dp[0], 8);
+        }
+      } else {
+        const int u = n - 4 * KS, kk = u / DB, db = u % DB;
+        dq[db] = mfma32(a, sb[kk], dq[db]);
+        if (u < 2 * DB) {
+#pragma unroll
+          for (int e = u * EQ; e < (u + 1) * EQ; ++e) dsv(1, e);
+          if ((u + 1) * EQ == 8) sb[2] = pack8(dp[1], 0);
+          if ((u + 1) * EQ == 16) sb[3] = pack8(dp[1], 8);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
     wait_async();
     __syncthreads();
   };
