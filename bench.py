@@ -57,6 +57,30 @@ def rank_for(F, w, cu, plan):
     return int(w.rank)
 
 
+def measured_traffic(entry, workload):
+    """HBM bytes per launch of a kernel from the committed counter summaries
+    (profiles/traffic_*.md, FETCH_SIZE and WRITE_SIZE scaled by a copy
+    kernel of known size); None when there is no record for this kernel and
+    workload, or when the kernel's sources changed since it was taken."""
+    import glob
+    import hashlib
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.md"))):
+        for line in open(path):
+            if not line.startswith("traffic-record:"):
+                continue
+            rec = json.loads(line.split(":", 1)[1])
+            if rec.get("entry") != entry or rec.get("workload") != workload:
+                continue
+            h = hashlib.sha256()
+            for src in rec["sources"]:
+                with open(os.path.join(ROOT, src), "rb") as f:
+                    h.update(f.read())
+            if h.hexdigest() != rec["sources_sha256"]:
+                return None
+            return int(rec["fetch_bytes_per_launch"]) + int(rec["write_bytes_per_launch"])
+    return None
+
+
 def cpu_baseline(cu, view_tables, x, w, seconds):
     """The oracle (fp32, as it stands) on whole document segments of the
     rank, forward + backward, until the time budget is used."""
@@ -237,14 +261,15 @@ def main():
     dom = max(range(len(names)), key=lambda i: acc[i])
     dn = names[dom]
     kind, amount = work[dn]
+    traffic = measured_traffic(dn, w.name)
     if kind == "mfma":
         ach = amount / (acc[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dn}
+                "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": traffic, "kernel": dn}
     else:
         ach = amount / (acc[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dn}
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": dn}
 
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
