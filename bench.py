@@ -4,8 +4,9 @@
 
 A step is the whole path once over one synthetic packed sequence: the shard
 plan and rank view (host, C++), the table upload, the KV gather that stands
-in for the sharding-aware receive, the local and received forward passes,
-their log-sum-exp merge, the backward preprocess and the key-major backward.
+in for the sharding-aware receive, the local and received forward partial
+passes (one launch), their log-sum-exp merge, the backward preprocess, and
+the key-major dK/dV and query-major dQ passes.
 Inputs are resident in HBM before timing starts. The metric counts useful
 FLOPs: 14 * d * Hq * pairs, pairs being the visible (query, key) pairs per
 head of the rank (sum of its shards' W_i); masked lanes never count.
@@ -176,7 +177,7 @@ def main():
     meta = torch.empty(int(info["meta_bytes"]) + 256, dtype=torch.uint8, device=dev)
     no_ws = torch.empty(0, dtype=torch.uint8, device=dev)
     dkdv_ws = torch.empty(view.workspace_size()[2], dtype=torch.uint8, device=dev)
-    names = ["kv_gather", "attn_fwd_local", "attn_fwd_recv", "lse_merge", "bwd_preprocess",
+    names = ["kv_gather", "attn_fwd_partials", "lse_merge", "bwd_preprocess",
              "attn_bwd_dkdv", "attn_bwd_dq"]
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
     acc = np.zeros(len(names))
@@ -190,24 +191,22 @@ def main():
         F.fc_kv_gather(v, k_pk, v_pk, k_loc, v_loc, k_recv, v_recv)
         ev[1].record()
         if tr:
-            F.fc_attn_fwd_partial(v, 0, q, k_loc, v_loc, 0.0, o_a, l_a)
+            # both partial passes (local keys, received keys) in one launch
+            F.fc_attn_fwd_partials(v, q, k_loc, v_loc, k_recv, v_recv, 0.0, o_a, l_a, o_b, l_b)
             ev[2].record()
-            F.fc_attn_fwd_partial(v, 1, q, k_recv, v_recv, 0.0, o_b, l_b)
-            ev[3].record()
             F.fc_lse_merge(o_a, l_a, o_b, l_b, o, None, lse)
         else:
             # no received KV: the local pass alone writes the final O and LSE
             F.fc_attn_fwd(v, q, k_loc, v_loc, k_recv, v_recv, 0.0, F.FC_TWO_PASS, o, None, lse, no_ws)
             ev[2].record()
-            ev[3].record()
-        ev[4].record()
+        ev[3].record()
         F.fc_bwd_preprocess(v, o, do, delta)
-        ev[5].record()
+        ev[4].record()
         F.fc_attn_bwd_dkdv(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dk_loc,
                            dv_loc, dk_recv, dv_recv, dkdv_ws)
-        ev[6].record()
+        ev[5].record()
         F.fc_attn_bwd_dq(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq)
-        ev[7].record()
+        ev[6].record()
 
     for _ in range(args.warmup):
         step(False)
@@ -237,8 +236,7 @@ def main():
     kv_rows = tq + tr
     work = {
         "kv_gather": ("hbm", 2 * 2 * kv_rows * hkv * d * 2),
-        "attn_fwd_local": ("mfma", 4.0 * d * hq * info["pairs_loc"]),
-        "attn_fwd_recv": ("mfma", 4.0 * d * hq * info["pairs_recv"]),
+        "attn_fwd_partials": ("mfma", 4.0 * d * hq * pairs),
         "lse_merge": ("hbm", tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4) if tr else 0),
         "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4)),
         # dK/dV pass: S, dP, dV, dK (8d per pair); dQ pass: S, dP again and dQ (6d)
@@ -250,7 +248,7 @@ def main():
         kind, amount = work[n]
         t = acc[i] * 1e-3
         if amount == 0 or acc[i] <= 0:
-            kernels[n] = {"ms": round(acc[i], 4), "skipped": "no received KV"}
+            kernels[n] = {"ms": round(acc[i], 4), "skipped": "no received KV (no merge)"}
             continue
         if kind == "mfma":
             a = amount / t / 1e12
@@ -278,7 +276,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.context}-token packed context, CP degree {w.cp}, "
                                f"{w.plan} plan, rank {rank}; {hq} query / {hkv} KV heads, d {d}; "
-                               "two-pass forward (local, received) + LSE merge, key-major backward",
+                               "two-pass forward (local and received partials in one launch) + LSE merge, "
+                               "key-major dK/dV and query-major dQ backward",
                    "t_q": tq, "t_recv": tr, "pairs_per_head": pairs,
                    "useful_tflop_per_step": round(useful / 1e12, 4),
                    "pct_of_bf16_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),

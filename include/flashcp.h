@@ -206,6 +206,16 @@ int fc_attn_fwd_partial(fc_view view, int32_t src, const void* q, const void* k_
                         const void* v_src, float scale, float* o_part, float* lse_part,
                         void* stream);
 
+/* Both partial passes in one launch (the two-pass forward's first step;
+ * fc_attn_fwd with FC_TWO_PASS uses it): local keys into o_loc/lse_loc,
+ * received keys into o_recv/lse_recv, with the shapes and the empty-row
+ * rule of fc_attn_fwd_partial; results are identical to the two separate
+ * calls. k_recv/v_recv may be NULL when the view receives no keys (the
+ * received partial is then O = 0, LSE = -inf everywhere). */
+int fc_attn_fwd_partials(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                         const void* k_recv, const void* v_recv, float scale, float* o_loc,
+                         float* lse_loc, float* o_recv, float* lse_recv, void* stream);
+
 /* LSE merge of two partial results over disjoint key sets, t rows of h
  * heads of dim d (d % 4 == 0): lse_out = ln(e^lse_a + e^lse_b), o =
  * e^(lse_a-lse_out) o_a + e^(lse_b-lse_out) o_b; a -inf partial has weight

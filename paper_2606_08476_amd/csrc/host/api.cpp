@@ -70,6 +70,23 @@ fck::FwdParams fwd_params(const View& v, const int32_t* items, const int32_t* pe
   return p;
 }
 
+// Both partial passes of the two-pass forward in one launch: the received
+// items write (o_recv, lse_recv), the local items (o_loc, lse_loc).
+int launch_partials(const View& v, const void* q, const void* k_loc, const void* v_loc,
+                    const void* k_recv, const void* v_recv, float scale, float* o_loc,
+                    float* lse_loc, float* o_recv, float* lse_recv, hipStream_t s) {
+  const int32_t* m = v.dev_meta;
+  fck::FwdParams p = fwd_params(v, m + v.off.fwd_two, m + v.off.perm_fwd_two,
+                                int64_t(v.fwd_two.size() / 8), q, k_loc, v_loc, k_recv, v_recv,
+                                scale);
+  p.o_f32 = o_loc;
+  p.lse = lse_loc;
+  p.n_first = int32_t(v.fwd_recv.size() / 8);
+  p.o_f32_first = o_recv;
+  p.lse_first = lse_recv;
+  return hip_status(fck::launch_fwd(p, v.d, v.heads_per_tile, false, s), "attn_fwd launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -139,6 +156,20 @@ int fc_attn_fwd_partial(fc_view view, int32_t src, const void* q, const void* k_
                     "attn_fwd launch");
 }
 
+int fc_attn_fwd_partials(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                         const void* k_recv, const void* v_recv, float scale, float* o_loc,
+                         float* lse_loc, float* o_recv, float* lse_recv, void* stream) {
+  fc::clear_error();
+  View* v;
+  if (int rc = check_view(view, v)) return rc;
+  if (v->t_q() == 0) return FC_OK;
+  if (!q || !k_loc || !v_loc || !o_loc || !lse_loc || !o_recv || !lse_recv ||
+      (v->t_recv() && (!k_recv || !v_recv)))
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  return launch_partials(*v, q, k_loc, v_loc, k_recv, v_recv, scale, o_loc, lse_loc, o_recv,
+                         lse_recv, reinterpret_cast<hipStream_t>(stream));
+}
+
 int fc_attn_fwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                 const void* k_recv, const void* v_recv, float scale, int32_t mode, void* o,
                 float* o_f32, float* lse, void* ws, size_t ws_bytes, void* stream) {
@@ -174,19 +205,7 @@ int fc_attn_fwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
   float* ob = reinterpret_cast<float*>(base + w.o_bytes);
   float* la = reinterpret_cast<float*>(base + 2 * w.o_bytes);
   float* lb = reinterpret_cast<float*>(base + 2 * w.o_bytes + w.l_bytes);
-  fck::FwdParams pl = fwd_params(*v, m + v->off.fwd_local, m + v->off.perm_fwd_local,
-                                 int64_t(v->fwd_local.size() / 8), q, k_loc, v_loc, nullptr,
-                                 nullptr, scale);
-  pl.o_f32 = oa;
-  pl.lse = la;
-  if (int rc = hip_status(fck::launch_fwd(pl, v->d, v->heads_per_tile, false, s), "local pass"))
-    return rc;
-  fck::FwdParams pr = fwd_params(*v, m + v->off.fwd_recv, m + v->off.perm_fwd_recv,
-                                 int64_t(v->fwd_recv.size() / 8), q, nullptr, nullptr, k_recv,
-                                 v_recv, scale);
-  pr.o_f32 = ob;
-  pr.lse = lb;
-  if (int rc = hip_status(fck::launch_fwd(pr, v->d, v->heads_per_tile, false, s), "recv pass"))
+  if (int rc = launch_partials(*v, q, k_loc, v_loc, k_recv, v_recv, scale, oa, la, ob, lb, s))
     return rc;
   return hip_status(fck::launch_lse_merge(oa, la, ob, lb, v->t_q(), v->hq, v->d,
                                           static_cast<uint16_t*>(o), o_f32, lse, s),

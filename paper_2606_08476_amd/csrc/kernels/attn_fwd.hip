@@ -44,7 +44,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int kvh = b % p.hkv;
   const int rest = b / p.hkv;
   const int hc = rest % p.head_chunks;
-  const int32_t* it = p.items + 8 * p.perm[rest / p.head_chunks];
+  const int item = p.perm[rest / p.head_chunks];
+  const int32_t* it = p.items + 8 * item;
+  float* const o_part = item < p.n_first ? p.o_f32_first : p.o_f32;
+  float* const lse_out = item < p.n_first ? p.lse_first : p.lse;
   const int q0 = it[0], q1 = it[1], r0 = it[2], r1 = it[3], l0 = it[4], l1 = it[5];
   const int ldiag = it[6];
 
@@ -202,10 +205,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
           packed.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
           *reinterpret_cast<uint2*>(p.o_bf16 + ob + dcol) = packed;
         }
-        if (!FINAL || p.o_f32) *reinterpret_cast<f32x4*>(p.o_f32 + ob + dcol) = v;
+        if (!FINAL || o_part) *reinterpret_cast<f32x4*>(o_part + ob + dcol) = v;
       }
     }
-    if (half == 0) p.lse[(size_t)h * p.t_q + qrow] = lse;
+    if (half == 0) lse_out[(size_t)h * p.t_q + qrow] = lse;
   }
 }
 

@@ -23,6 +23,11 @@ struct FwdParams {
   float* o_f32;
   float* lse;               // [hq, t_q]
   int32_t t_q;
+  // partial outputs of items with index < n_first (0: none), used when one
+  // launch runs both partial passes
+  int32_t n_first;
+  float* o_f32_first;
+  float* lse_first;
 };
 
 struct BwdParams {

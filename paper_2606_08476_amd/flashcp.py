@@ -29,7 +29,7 @@ EXPORTS = [
     "fc_plan_per_doc", "fc_plan_whole_lpt", "fc_plan_hybrid", "fc_plan_validate",
     "fc_plan_stats", "fc_view_create", "fc_view_get_info", "fc_view_export", "fc_view_bind",
     "fc_view_destroy", "fc_workspace_size", "fc_kv_gather", "fc_attn_fwd",
-    "fc_attn_fwd_partial", "fc_lse_merge", "fc_attn_bwd", "fc_bwd_preprocess",
+    "fc_attn_fwd_partial", "fc_attn_fwd_partials", "fc_lse_merge", "fc_attn_bwd", "fc_bwd_preprocess",
     "fc_attn_bwd_pass", "fc_attn_bwd_dkdv", "fc_attn_bwd_dq", "fc_last_error",
 ]
 
@@ -91,6 +91,7 @@ def lib():
             "fc_kv_gather": [P, P, P, C.c_int64, P, P, P, P, P],
             "fc_attn_fwd": [P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, C.c_size_t, P],
             "fc_attn_fwd_partial": [P, C.c_int32, P, P, P, C.c_float, P, P, P],
+            "fc_attn_fwd_partials": [P, P, P, P, P, P, C.c_float, P, P, P, P, P],
             "fc_lse_merge": [P, P, P, P, C.c_int32, C.c_int32, C.c_int32, P, P, P, P],
             "fc_attn_bwd": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P, C.c_size_t, P],
             "fc_bwd_preprocess": [P, P, P, P, P],
@@ -316,6 +317,21 @@ def fc_attn_fwd_partial(view: View, src, q, k_src, v_src, scale, o_part, lse_par
         view.handle, int(src), _ptr(q, (tq, hq, d), bf, "q"), _ptr(k_src, (tk, hkv, d), bf, "k_src"),
         _ptr(v_src, (tk, hkv, d), bf, "v_src"), float(scale), _ptr(o_part, (tq, hq, d), f32, "o_part"),
         _ptr(lse_part, (hq, tq), f32, "lse_part"), _stream()))
+
+
+def fc_attn_fwd_partials(view: View, q, k_loc, v_loc, k_recv, v_recv, scale, o_loc, lse_loc,
+                         o_recv, lse_recv):
+    import torch
+    i = view.info
+    bf, f32 = torch.bfloat16, torch.float32
+    tq, tr, hq, hkv, d = i["t_q"], i["t_recv"], i["hq"], i["hkv"], i["d"]
+    _check(lib().fc_attn_fwd_partials(
+        view.handle, _ptr(q, (tq, hq, d), bf, "q"), _ptr(k_loc, (tq, hkv, d), bf, "k_loc"),
+        _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
+        _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), float(scale),
+        _ptr(o_loc, (tq, hq, d), f32, "o_loc"), _ptr(lse_loc, (hq, tq), f32, "lse_loc"),
+        _ptr(o_recv, (tq, hq, d), f32, "o_recv"), _ptr(lse_recv, (hq, tq), f32, "lse_recv"),
+        _stream()))
 
 
 def fc_lse_merge(o_a, lse_a, o_b, lse_b, o_bf16, o_f32, lse_out):

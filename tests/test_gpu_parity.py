@@ -160,6 +160,19 @@ def test_partial_passes_and_merge(key, dev):
         say(f"[gpu] {key} partial src={src}: O {eo:.3e} LSE {el:.3e}")
         assert eo <= O_TOL and el <= LSE_TOL
         outs.append((Oref, Lref))
+    # both partial passes in one launch give the same bits as the two calls
+    sep = []
+    for src, kg, vg in ((0, r.k_loc, r.v_loc), (1, r.k_recv, r.v_recv)):
+        op = torch.empty(tq, hq, d, dtype=torch.float32, device=dev)
+        lp = torch.empty(hq, tq, dtype=torch.float32, device=dev)
+        F.fc_attn_fwd_partial(r.v, src, r.q, kg, vg, 0.0, op, lp)
+        sep.append((op, lp))
+    o2 = [torch.full((tq, hq, d), float("nan"), device=dev) for _ in range(2)]
+    l2 = [torch.full((hq, tq), float("nan"), device=dev) for _ in range(2)]
+    F.fc_attn_fwd_partials(r.v, r.q, r.k_loc, r.v_loc, r.k_recv, r.v_recv, 0.0, o2[0], l2[0], o2[1], l2[1])
+    torch.cuda.synchronize()
+    for (op, lp), oc, lc in zip(sep, o2, l2):
+        assert torch.equal(op, oc) and torch.equal(lp, lc)
     # the merge kernel on the oracle's partials against the oracle's merge
     (Oa, La), (Ob, Lb) = outs
     Om, Lm = A.lse_merge(Oa, La, Ob, Lb)

@@ -173,6 +173,7 @@ def test_kernel_calls_rejected_before_launch():
     assert lib.fc_attn_bwd(h, *([1] * 8), 0.0, *([1] * 5), None, 0, None) == -5
     assert lib.fc_attn_bwd_dkdv(h, *([1] * 8), 0.0, *([1] * 4), None, 0, None) == -5
     assert lib.fc_attn_fwd_partial(h, 0, 1, 1, 1, 0.0, 1, 1, None) == -5
+    assert lib.fc_attn_fwd_partials(h, 1, 1, 1, 1, 1, 0.0, 1, 1, 1, 1, None) == -5
     assert lib.fc_lse_merge(1, 1, 1, 1, 4, 2, 96, 1, None, 1, None) == -4
     assert lib.fc_lse_merge(1, 1, 1, 1, -1, 2, 64, 1, None, 1, None) == -1
     f, b, k = v.workspace_size(F.FC_TWO_PASS)
