@@ -177,8 +177,7 @@ def main():
     meta = torch.empty(int(info["meta_bytes"]) + 256, dtype=torch.uint8, device=dev)
     no_ws = torch.empty(0, dtype=torch.uint8, device=dev)
     dkdv_ws = torch.empty(view.workspace_size()[2], dtype=torch.uint8, device=dev)
-    names = ["kv_gather", "attn_fwd_partials", "lse_merge", "bwd_preprocess",
-             "attn_bwd_dkdv", "attn_bwd_dq"]
+    names = ["kv_gather", "attn_fwd_partials", "lse_merge", "bwd_preprocess", "attn_bwd"]
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
     acc = np.zeros(len(names))
     kept = []
@@ -202,11 +201,10 @@ def main():
         ev[3].record()
         F.fc_bwd_preprocess(v, o, do, delta)
         ev[4].record()
-        F.fc_attn_bwd_dkdv(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dk_loc,
+        # dK/dV (key-major) and dQ (query-major) workgroups in one launch
+        F.fc_attn_bwd_pass(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq, dk_loc,
                            dv_loc, dk_recv, dv_recv, dkdv_ws)
         ev[5].record()
-        F.fc_attn_bwd_dq(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq)
-        ev[6].record()
 
     for _ in range(args.warmup):
         step(False)
@@ -239,9 +237,8 @@ def main():
         "attn_fwd_partials": ("mfma", 4.0 * d * hq * pairs),
         "lse_merge": ("hbm", tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4) if tr else 0),
         "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4)),
-        # dK/dV pass: S, dP, dV, dK (8d per pair); dQ pass: S, dP again and dQ (6d)
-        "attn_bwd_dkdv": ("mfma", 8.0 * d * hq * pairs),
-        "attn_bwd_dq": ("mfma", 6.0 * d * hq * pairs),
+        # backward: dK/dV part S, dP, dV, dK (8d per pair) + dQ part S, dP again, dQ (6d)
+        "attn_bwd": ("mfma", 14.0 * d * hq * pairs),
     }
     kernels = {}
     for i, n in enumerate(names):

@@ -87,6 +87,71 @@ int launch_partials(const View& v, const void* q, const void* k_loc, const void*
   return hip_status(fck::launch_fwd(p, v.d, v.heads_per_tile, false, s), "attn_fwd launch");
 }
 
+fck::BwdParams bwd_params(const View& v, const void* q, const void* k_loc, const void* v_loc,
+                          const void* k_recv, const void* v_recv, const float* lse,
+                          const float* delta, const void* dout, float scale, float* dk_loc,
+                          float* dv_loc, float* dk_recv, float* dv_recv, void* ws, size_t part) {
+  const int32_t* m = v.dev_meta;
+  fck::BwdParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.dout = static_cast<const uint16_t*>(dout);
+  p.lse = lse;
+  p.delta = delta;
+  p.k_loc = static_cast<const uint16_t*>(k_loc);
+  p.v_loc = static_cast<const uint16_t*>(v_loc);
+  p.k_recv = static_cast<const uint16_t*>(k_recv);
+  p.v_recv = static_cast<const uint16_t*>(v_recv);
+  p.items = m + v.off.bwd_launch;
+  p.perm = m + v.off.perm_bwd_launch;
+  p.lim = m + v.off.lim;
+  p.n_items = int32_t(v.bwd_launch.size() / 8);
+  p.part_k = static_cast<float*>(ws);
+  p.part_v = part ? reinterpret_cast<float*>(static_cast<char*>(ws) + part / 2) : nullptr;
+  p.hq = v.hq;
+  p.hkv = v.hkv;
+  p.group = v.hq / v.hkv;
+  p.scale = resolve_scale(scale, v.d);
+  p.dk_loc = dk_loc;
+  p.dv_loc = dv_loc;
+  p.dk_recv = dk_recv;
+  p.dv_recv = dv_recv;
+  p.t_q = v.t_q();
+  return p;
+}
+
+fck::DqParams dq_params(const View& v, const void* q, const void* k_loc, const void* v_loc,
+                        const void* k_recv, const void* v_recv, const float* lse,
+                        const float* delta, const void* dout, float scale, float* dq) {
+  const int32_t* m = v.dev_meta;
+  fck::DqParams d{};
+  d.q = static_cast<const uint16_t*>(q);
+  d.dout = static_cast<const uint16_t*>(dout);
+  d.lse = lse;
+  d.delta = delta;
+  d.k_loc = static_cast<const uint16_t*>(k_loc);
+  d.v_loc = static_cast<const uint16_t*>(v_loc);
+  d.k_recv = static_cast<const uint16_t*>(k_recv);
+  d.v_recv = static_cast<const uint16_t*>(v_recv);
+  d.items = m + v.off.fwd_fused;
+  d.perm = m + v.off.perm_fwd_fused;
+  d.n_items = int32_t(v.fwd_fused.size() / 8);
+  d.hq = v.hq;
+  d.hkv = v.hkv;
+  d.group = v.hq / v.hkv;
+  d.head_chunks = d.group / v.heads_per_tile;
+  d.scale = resolve_scale(scale, v.d);
+  d.dq = dq;
+  d.t_q = v.t_q();
+  return d;
+}
+
+int launch_reduce(const View& v, const fck::BwdParams& p, hipStream_t s) {
+  return hip_status(fck::launch_bwd_reduce(v.dev_meta + v.off.bwd_reduce,
+                                           int32_t(v.bwd_reduce.size() / 8), p.part_k, p.part_v,
+                                           v.hkv, v.d, p.dk_loc, p.dv_loc, p.dk_recv, p.dv_recv, s),
+                    "attn_bwd reduce launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -256,37 +321,11 @@ int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void*
   if (need && (!ws || ws_bytes < need))
     return fail(FC_ERR_WORKSPACE, "dK/dV workspace of " + std::to_string(ws_bytes) +
                                       " bytes, need " + std::to_string(need));
-  const int32_t* m = v->dev_meta;
-  fck::BwdParams p{};
-  p.q = static_cast<const uint16_t*>(q);
-  p.dout = static_cast<const uint16_t*>(dout);
-  p.lse = lse;
-  p.delta = delta;
-  p.k_loc = static_cast<const uint16_t*>(k_loc);
-  p.v_loc = static_cast<const uint16_t*>(v_loc);
-  p.k_recv = static_cast<const uint16_t*>(k_recv);
-  p.v_recv = static_cast<const uint16_t*>(v_recv);
-  p.items = m + v->off.bwd_launch;
-  p.perm = m + v->off.perm_bwd_launch;
-  p.lim = m + v->off.lim;
-  p.n_items = int32_t(v->bwd_launch.size() / 8);
-  p.part_k = static_cast<float*>(ws);
-  p.part_v = need ? reinterpret_cast<float*>(static_cast<char*>(ws) + need / 2) : nullptr;
-  p.hq = v->hq;
-  p.hkv = v->hkv;
-  p.group = v->hq / v->hkv;
-  p.scale = resolve_scale(scale, v->d);
-  p.dk_loc = dk_loc;
-  p.dv_loc = dv_loc;
-  p.dk_recv = dk_recv;
-  p.dv_recv = dv_recv;
-  p.t_q = v->t_q();
+  fck::BwdParams p = bwd_params(*v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
+                                dk_loc, dv_loc, dk_recv, dv_recv, ws, need);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (int rc = hip_status(fck::launch_bwd(p, v->d, s), "attn_bwd dK/dV launch")) return rc;
-  return hip_status(fck::launch_bwd_reduce(m + v->off.bwd_reduce, int32_t(v->bwd_reduce.size() / 8),
-                                           p.part_k, p.part_v, v->hkv, v->d, dk_loc, dv_loc,
-                                           dk_recv, dv_recv, s),
-                    "attn_bwd reduce launch");
+  return launch_reduce(*v, p, s);
 }
 
 int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v_loc,
@@ -299,26 +338,7 @@ int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v
   if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dq ||
       (v->t_recv() && (!k_recv || !v_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  const int32_t* m = v->dev_meta;
-  fck::DqParams d{};
-  d.q = static_cast<const uint16_t*>(q);
-  d.dout = static_cast<const uint16_t*>(dout);
-  d.lse = lse;
-  d.delta = delta;
-  d.k_loc = static_cast<const uint16_t*>(k_loc);
-  d.v_loc = static_cast<const uint16_t*>(v_loc);
-  d.k_recv = static_cast<const uint16_t*>(k_recv);
-  d.v_recv = static_cast<const uint16_t*>(v_recv);
-  d.items = m + v->off.fwd_fused;
-  d.perm = m + v->off.perm_fwd_fused;
-  d.n_items = int32_t(v->fwd_fused.size() / 8);
-  d.hq = v->hq;
-  d.hkv = v->hkv;
-  d.group = v->hq / v->hkv;
-  d.head_chunks = d.group / v->heads_per_tile;
-  d.scale = resolve_scale(scale, v->d);
-  d.dq = dq;
-  d.t_q = v->t_q();
+  fck::DqParams d = dq_params(*v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq);
   return hip_status(fck::launch_bwd_dq(d, v->d, v->heads_per_tile,
                                        reinterpret_cast<hipStream_t>(stream)),
                     "attn_bwd dQ launch");
@@ -332,12 +352,23 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
-  if (!dq) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  if (int rc = fc_attn_bwd_dkdv(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
-                                dk_loc, dv_loc, dk_recv, dv_recv, ws, ws_bytes, stream))
+  if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dq || !dk_loc || !dv_loc ||
+      (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
+    return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  const size_t need = part_ws(*v);
+  if (need && (!ws || ws_bytes < need))
+    return fail(FC_ERR_WORKSPACE, "dK/dV workspace of " + std::to_string(ws_bytes) +
+                                      " bytes, need " + std::to_string(need));
+  // dK/dV and dQ workgroups in one launch, then the reduce of split key tiles
+  const fck::BwdParams p = bwd_params(*v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout,
+                                      scale, dk_loc, dv_loc, dk_recv, dv_recv, ws, need);
+  const fck::DqParams d = dq_params(*v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout,
+                                    scale, dq);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (int rc = hip_status(fck::launch_bwd_grid(p, d, v->d, v->heads_per_tile, s),
+                          "attn_bwd launch"))
     return rc;
-  return fc_attn_bwd_dq(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq,
-                        stream);
+  return launch_reduce(*v, p, s);
 }
 
 int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,

@@ -1,240 +1,50 @@
-// Backward attention, dK/dV part (gfx950), key-major.
-//
-// One workgroup (4 waves) owns a tile of 128 keys of one source (local or
-// received) and one KV head; wave w owns keys 32w..32w+31, so dK and dV for
-// the tile accumulate in registers, summed over every query head of the
-// group (grouped-query attention) and every query tile that sees the keys.
-// K sits in LDS, V in registers. The (query head, 32-query tile) iterations
-// are software-pipelined: the next tile's Q and dO are copied from HBM
-// straight into a second LDS buffer (asynchronous loads) while the current
-// one is computed. Per iteration:
-//   S  = Q K^T, dP = dO V^T     MFMA (Q, dO, K from LDS, V from registers);
-//   P  = exp(S - LSE), dS = P (dP - D)   D = rowsum(dO * O) from the
-//                               preprocess kernel, LSE the merged forward LSE;
-//   dV += P^T dO, dK += dS^T Q  P and dS from registers, dO/Q read from LDS
-//                               with transpose reads.
-// Masking (edge tiles only): local keys are causal in local order; a
-// received key is seen by a query iff its index is below the query's
-// receive limit.
-#include "common.hpp"
-#include "launch.hpp"
-
-#include <type_traits>
+// Backward attention kernels (gfx950): the key-major dK/dV kernel, and the
+// whole backward pass (dK/dV and dQ workgroups) in one launch. The
+// per-workgroup bodies are in bwd_dkdv.hpp and bwd_dq.hpp.
+#include "bwd_dkdv.hpp"
+#include "bwd_dq.hpp"
 
 namespace fck {
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_bwd_kernel(BwdParams p) {
-  constexpr int BN = 128;       // keys per workgroup
-  constexpr int BM = 32;        // queries per iteration
-  constexpr int KS = D / 16;
-  constexpr int DB = D / 32;
-  constexpr uint32_t KT = BN * D * 2;  // bytes of the key tile
-  constexpr uint32_t QT = BM * D * 2;  // bytes of a Q or dO tile
-  // LDS layout (bytes): per buffer b, LSE at 256*3b, delta at +256, receive
-  // limits at +512 (a wave-wide copy each, the first BM entries used); then
-  // the key tile; then Q and dO of buffer 0 and of buffer 1. The loop is
-  // unrolled by two, so every read names its buffer with a compile-time
-  // offset (all below 64 KiB, the reach of the offset field).
-  constexpr uint32_t OK = 6 * 256;
-  constexpr uint32_t OQ0 = OK + KT, OO0 = OQ0 + QT, OQ1 = OO0 + QT, OO1 = OQ1 + QT;
-  __shared__ __attribute__((aligned(16))) char smem[OO1 + QT];
+  __shared__ __attribute__((aligned(16))) char smem[DkdvLds<D>::bytes];
+  dkdv_tile<D>(p, blockIdx.x, smem);
+}
 
-  const int lane = threadIdx.x & 63, wave = wave_id();
-  const int half = lane >> 5;
+// The whole backward pass in one launch: the first n_dkdv workgroups take
+// key tiles (dK/dV), the others query tiles (dQ); the dQ workgroups start
+// as dK/dV ones finish, so neither pass leaves a tail of its own.
+template <int D, int HPW>
+__global__ __launch_bounds__(256, 2) void attn_bwd_grid_kernel(BwdParams bp, DqParams dp, int n_dkdv) {
+  constexpr uint32_t kBytes = DkdvLds<D>::bytes > DqLds<D>::bytes ? DkdvLds<D>::bytes : DqLds<D>::bytes;
+  __shared__ __attribute__((aligned(16))) char smem[kBytes];
   const int b = blockIdx.x;
-  const int kvh = b % p.hkv;
-  const int32_t* it = p.items + 8 * p.perm[b / p.hkv];  // launch list
-  const int k0 = it[0], k1 = it[1], q0 = it[2], q1 = it[3], qfull = it[4], src = it[5];
-  const u16* Kg = src ? p.k_recv : p.k_loc;
-  const u16* Vg = src ? p.v_recv : p.v_loc;
-  float* dKg = src ? p.dk_recv : p.dk_loc;
-  float* dVg = src ? p.dv_recv : p.dv_loc;
-  const size_t kvs = size_t(p.hkv) * D, kvo = size_t(kvh) * D;
+  if (b < n_dkdv)
+    dkdv_tile<D>(bp, b, smem);
+  else
+    dq_tile<D, HPW>(dp, b - n_dkdv, smem);
+}
 
-  // key tile (rows past k1 repeat the last key; they are masked)
-  TileLoader<D, BN>(p.hkv * D).load_at(lds_addr(smem) + OK, Kg + size_t(k0) * kvs + kvo, k1 - k0);
-  const int kidx = k0 + 32 * wave + (lane & 31);  // this lane's key
-  const bool kvalid = kidx < k1;
-  // V rows of this lane's key as the B operand of dP = dO V^T
-  bf16x8 vreg[KS];
-  {
-    const u16* vp = Vg + size_t(kidx) * kvs + kvo + 8 * half;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      vreg[ks] = kvalid ? *reinterpret_cast<const bf16x8*>(vp + 16 * ks) : zero8();
+template <int D>
+static hipError_t launch_grid_d(const BwdParams& bp, const DqParams& dp, int hpw, hipStream_t s) {
+  const int n_dkdv = bp.n_items * bp.hkv;
+  const dim3 grid(unsigned(n_dkdv + dp.n_items * dp.hkv * dp.head_chunks)), block(256);
+  switch (hpw) {
+    case 1: hipLaunchKernelGGL((attn_bwd_grid_kernel<D, 1>), grid, block, 0, s, bp, dp, n_dkdv); break;
+    case 2: hipLaunchKernelGGL((attn_bwd_grid_kernel<D, 2>), grid, block, 0, s, bp, dp, n_dkdv); break;
+    case 4: hipLaunchKernelGGL((attn_bwd_grid_kernel<D, 4>), grid, block, 0, s, bp, dp, n_dkdv); break;
+    default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
 
-  const int ntile = (q1 - q0 + BM - 1) / BM;
-  const int n_it = ntile * p.group;
-
-  // next iteration: Q/dO tiles, LSE, D and receive limits, all copied from
-  // HBM straight into LDS (rows past q1 repeat the last query; masked)
-  const TileLoader<D, BM> ldq(p.hq * D);
-  auto fetch = [&](int i_, int buf) {
-    const int h = kvh * p.group + i_ / ntile;
-    const int t0 = q0 + (i_ % ntile) * BM;
-    const size_t base = (size_t(t0) * p.hq + h) * D;
-    const uint32_t sb = lds_addr(smem);
-    ldq.load_at(sb + (buf ? OQ1 : OQ0), p.q + base, q1 - t0);
-    ldq.load_at(sb + (buf ? OO1 : OO0), p.dout + base, q1 - t0);
-    const uint32_t qoff = 4u * uint32_t(min(t0 + (lane & 31), q1 - 1));
-    const uint32_t sm = sb + 768u * buf;
-    if (wave == 0)
-      lds_copy4(p.lse + (size_t)h * p.t_q, qoff, sm);
-    else if (wave == 1)
-      lds_copy4(p.delta + (size_t)h * p.t_q, qoff, sm + 256);
-    else if (wave == 2 && src)
-      lds_copy4(p.lim, qoff, sm + 512);
-  };
-
-  // per-lane LDS byte offsets (swizzled tiles): row reads of a 32-row block
-  // (Q and dO tiles; the key rows are the same plus this wave's block) and
-  // transpose reads; a k-step or column block is an XOR of a constant
-  uint32_t pr = 2u * uint32_t(row_base<D>(0, lane));
-  uint32_t pt = 2u * uint32_t(tr_base<D>(lane));
-  const uint32_t kofs = OK + uint32_t(wave) * 64u * D;  // this wave's key rows
-
-  f32x16 dk[DB], dv[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    dk[db] = zero16();
-    dv[db] = zero16();
-  }
-  const bool kfull = k1 - k0 == BN;
-  const float sl2 = p.scale * kLog2e;
-  // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
-  const int kx = kvalid ? kidx : 0x7fffffff;  // never below a receive limit
-
-  if (n_it > 0) fetch(0, 0);
-  wait_async();
-  __syncthreads();
-
-  // One query tile. The 4*KS... MFMAs of the step run as one software
-  // pipeline of slots, in this order:
-  //   S = Q K^T (KS slots); dP = dO V^T (KS slots, each also computing part of
-  //   P = exp(S - LSE)); dV += P^T dO (2*DB slots, each also computing part
-  //   of dS = P (dP - D)); dK += dS^T Q (2*DB slots).
-  // Each slot issues the LDS reads of the slot two ahead, its MFMA, and its
-  // share of the vector work, which then runs while the MFMA does; a
-  // scheduling barrier after each slot keeps this order.
-  constexpr int NS = 2 * KS + 4 * DB;       // slots per step
-  constexpr int EP = 16 / KS, ES = 8 / DB;  // P / dS elements per slot
-  auto step = [&](int i_, auto bufc) {
-    constexpr int B = decltype(bufc)::value;
-    constexpr uint32_t QO = B ? OQ1 : OQ0, OO = B ? OO1 : OO0, SO = 768u * B;
-    const int t0 = q0 + (i_ % ntile) * BM;
-    if (i_ + 1 < n_it) fetch(i_ + 1, B ^ 1);
-    pr = opaque(pr);
-    pt = opaque(pt);
-    // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
-    // (register 4g + j): rows cq < hiq exist; on a local diagonal the key is
-    // seen by rows cq >= lo; on a received diagonal by rows whose receive
-    // limit exceeds the key index
-    const bool diag = t0 < qfull;
-    const int hiq = q1 - t0 - 4 * half;
-    const int lo = !kvalid ? 0x40000000 : (diag && !src) ? kidx - t0 - 4 * half : -0x40000000;
-    const int kl = (diag && src) ? kx : -0x7fffffff;
-
-    f32x16 sacc = zero16(), dpacc = zero16();
-    bf16x8 ra[3], rb[3], pa[2], sa[2];
-    f32x4 l4[4], d4[4];
-    int4 m4[4];
-    // LDS operand reads of slot n into ring entry n % 3
-    auto rd = [&](int n) {
-      bf16x8& a = ra[n % 3];
-      if (n < KS) {
-        const uint32_t r = pr ^ (n << 5);
-        a = lds_b128(smem, r, QO);
-        rb[n % 3] = lds_b128(smem, r + kofs, 0);
-      } else if (n < 2 * KS) {
-        a = lds_b128(smem, pr ^ ((n - KS) << 5), OO);
-      } else {
-        const int u = n < 2 * KS + 2 * DB ? n - 2 * KS : n - 2 * KS - 2 * DB;
-        const int kh = u / DB, db = u % DB;
-        const uint32_t base = (n < 2 * KS + 2 * DB ? OO : QO) + kh * 32 * D;
-        const uint32_t t0_ = pt ^ (db << 6), t1_ = (pt ^ ((db << 6) | 32)) + 16 * D;
-        a = cat8(lds_tr(smem, t0_, base), lds_tr(smem, t1_, base));
-      }
-    };
-    rd(0);
-    rd(1);
-#pragma unroll
-    for (int n = 0; n < NS; ++n) {
-      if (n + 2 < NS) rd(n + 2);
-      if (n == KS - 2) {  // LSE, delta and limits of the 16 rows
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          l4[g] = *reinterpret_cast<const f32x4*>(smem + SO + 4 * (8 * g + 4 * half));
-          m4[g] = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
-        }
-      }
-      if (n == KS - 1) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-          d4[g] = *reinterpret_cast<const f32x4*>(smem + SO + 256 + 4 * (8 * g + 4 * half));
-      }
-      const bf16x8& a = ra[n % 3];
-      if (n < KS) {
-        sacc = mfma32(a, rb[n % 3], sacc);
-      } else if (n < 2 * KS) {
-        dpacc = mfma32(a, vreg[n - KS], dpacc);
-#pragma unroll
-        for (int e = (n - KS) * EP; e < (n - KS + 1) * EP; ++e) {
-          const int g = e >> 2, j = e & 3, cq = 8 * g + j;
-          const int lim = j == 0 ? m4[g].x : j == 1 ? m4[g].y : j == 2 ? m4[g].z : m4[g].w;
-          const float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], sl2, -l4[g][j] * kLog2e));
-          sacc[e] = ((cq >= lo) & (cq < hiq) & (kl < lim)) ? pij : 0.f;
-        }
-        if ((n - KS + 1) * EP == 8) pa[0] = pack8(sacc, 0);
-        if ((n - KS + 1) * EP == 16) pa[1] = pack8(sacc, 8);
-      } else if (n < 2 * KS + 2 * DB) {
-        const int u = n - 2 * KS, kh = u / DB, db = u % DB;
-        dv[db] = mfma32(pa[kh], a, dv[db]);
-#pragma unroll
-        for (int e = u * ES; e < (u + 1) * ES; ++e)
-          dpacc[e] = sacc[e] * (dpacc[e] - d4[e >> 2][e & 3]);
-        if ((u + 1) * ES == 8) sa[0] = pack8(dpacc, 0);
-        if ((u + 1) * ES == 16) sa[1] = pack8(dpacc, 8);
-      } else {
-        const int u = n - 2 * KS - 2 * DB, kh = u / DB, db = u % DB;
-        dk[db] = mfma32(sa[kh], a, dk[db]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    wait_async();
-    __syncthreads();
-  };
-  for (int i_ = 0; i_ < n_it; i_ += 2) {
-    step(i_, std::integral_constant<int, 0>());
-    if (i_ + 1 < n_it) step(i_ + 1, std::integral_constant<int, 1>());
-  }
-
-  // dK/dV of this tile, or of this part of a split tile (partial slot)
-  const int slot = it[7];
-  float* outK = dKg;
-  float* outV = dVg;
-  size_t rs = size_t(p.hkv) * D, base = size_t(kvh) * D;
-  int r0 = k0;
-  if (slot >= 0) {
-    outK = p.part_k;
-    outV = p.part_v;
-    rs = D;
-    base = (size_t(slot) * p.hkv + kvh) * BN * D;
-    r0 = 0;
-  }
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int r = 32 * wave + 8 * (i >> 2) + 4 * half + (i & 3);
-      if (k0 + r < k1) {
-        const size_t g = base + size_t(r0 + r) * rs + 32 * db + (lane & 31);
-        outK[g] = p.scale * dk[db][i];
-        outV[g] = dv[db][i];
-      }
-    }
-  }
+hipError_t launch_bwd_grid(const BwdParams& bp, const DqParams& dp, int d, int heads_per_tile,
+                           hipStream_t s) {
+  if (bp.n_items == 0 && dp.n_items == 0) return hipSuccess;
+  if (d == 64) return launch_grid_d<64>(bp, dp, heads_per_tile, s);
+  if (d == 128) return launch_grid_d<128>(bp, dp, heads_per_tile, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_bwd(const BwdParams& p, int d, hipStream_t s) {

@@ -76,6 +76,9 @@ hipError_t launch_fwd(const FwdParams& p, int d, int heads_per_tile, bool final_
                       hipStream_t s);
 hipError_t launch_bwd_dq(const DqParams& p, int d, int heads_per_tile, hipStream_t s);
 hipError_t launch_bwd(const BwdParams& p, int d, hipStream_t s);
+// dK/dV and dQ in one launch (dK/dV workgroups first)
+hipError_t launch_bwd_grid(const BwdParams& bp, const DqParams& dp, int d, int heads_per_tile,
+                           hipStream_t s);
 hipError_t launch_bwd_reduce(const int32_t* entries, int32_t n, const float* part_k,
                              const float* part_v, int32_t hkv, int32_t d, float* dk_loc,
                              float* dv_loc, float* dk_recv, float* dv_recv, hipStream_t s);

@@ -1,7 +1,7 @@
 """GPU parity at the workloads' full sizes, in the launch configuration the
-benchmark times (gather, local and received forward passes, LSE merge,
-preprocess, dK/dV pass, dQ pass), against the fp64 oracle on outputs it
-can compute one by one:
+benchmark times (gather; both forward partial passes in one launch; LSE
+merge; preprocess; dK/dV and dQ workgroups in one launch), against the fp64
+oracle on outputs it can compute one by one:
 
 * O, LSE and dQ on sampled query rows (every head), including the first and
   last rows of pieces;
@@ -87,20 +87,24 @@ def test_full_size(name, dev):
     F.fc_kv_gather(v, xd["k_pk"], xd["v_pk"], kl, vl, kr, vr)
     oa, ob, la, lb = e(tq, hq, d), e(tq, hq, d), e(hq, tq), e(hq, tq)
     o, lse, delta = e(tq, hq, d, dt=bf), e(hq, tq), e(hq, tq)
-    F.fc_attn_fwd_partial(v, 0, xd["q"], kl, vl, 0.0, oa, la)
     if tr:
-        F.fc_attn_fwd_partial(v, 1, xd["q"], kr, vr, 0.0, ob, lb)
+        F.fc_attn_fwd_partials(v, xd["q"], kl, vl, kr, vr, 0.0, oa, la, ob, lb)
         F.fc_lse_merge(oa, la, ob, lb, o, None, lse)
     else:
         ws = torch.empty(1, dtype=torch.uint8, device=dev)
         F.fc_attn_fwd(v, xd["q"], kl, vl, kr, vr, 0.0, F.FC_TWO_PASS, o, None, lse, ws)
     F.fc_bwd_preprocess(v, o, xd["do"], delta)
     dq, dkl, dvl, dkr, dvr = e(tq, hq, d), e(tq, hkv, d), e(tq, hkv, d), e(tr, hkv, d), e(tr, hkv, d)
-    ws = torch.empty(v.workspace_size()[2], dtype=torch.uint8, device=dev)
-    F.fc_attn_bwd_dkdv(v, xd["q"], kl, vl, kr, vr, lse, delta, xd["do"], 0.0, dkl, dvl, dkr, dvr, ws)
-    F.fc_attn_bwd_dq(v, xd["q"], kl, vl, kr, vr, lse, delta, xd["do"], 0.0, dq)
+    ws = torch.empty(max(v.workspace_size()[2], 1), dtype=torch.uint8, device=dev)
+    F.fc_attn_bwd_pass(v, xd["q"], kl, vl, kr, vr, lse, delta, xd["do"], 0.0, dq, dkl, dvl, dkr, dvr, ws)
+    # the separate dK/dV and dQ kernels give the same bits
+    dq2, dkl2, dvl2, dkr2, dvr2 = (torch.empty_like(t) for t in (dq, dkl, dvl, dkr, dvr))
+    F.fc_attn_bwd_dkdv(v, xd["q"], kl, vl, kr, vr, lse, delta, xd["do"], 0.0, dkl2, dvl2, dkr2, dvr2, ws)
+    F.fc_attn_bwd_dq(v, xd["q"], kl, vl, kr, vr, lse, delta, xd["do"], 0.0, dq2)
     torch.cuda.synchronize()
     say(f"[gpu-full] {name}: GPU done")
+    for a, b in ((dq, dq2), (dkl, dkl2), (dvl, dvl2), (dkr, dkr2), (dvr, dvr2)):
+        assert torch.equal(a, b)
 
     assert torch.equal(kl.cpu(), x["k_loc"]) and torch.equal(vl.cpu(), x["v_loc"])
     assert torch.equal(kr.cpu(), x["k_recv"]) and torch.equal(vr.cpu(), x["v_recv"])
