@@ -38,7 +38,116 @@ def parse():
     ap.add_argument("--mode", choices=["two_pass"], default="two_pass")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle baseline sample (0 disables it)")
+    ap.add_argument("--study", choices=["planner", "granularity"], default=None,
+                    help="instead of the step benchmark: the planner-quality study (host "
+                         "only) or the shard-granularity kernel study; JSON lines, then a table")
+    ap.add_argument("--seeds", type=int, default=5, help="length seeds per planner-study row")
     return ap.parse_args()
+
+
+# ------------------------------------------------------------------ studies
+
+PLANNERS = ["per_seq", "per_doc", "whole_lpt", "hybrid"]
+
+
+def run_planner(F, name, cu, cp):
+    if name == "per_seq":
+        return F.fc_plan_per_seq(cu, cp)
+    if name == "per_doc":
+        return F.fc_plan_per_doc(cu, cp)
+    if name == "whole_lpt":
+        return F.fc_plan_whole_lpt(cu, cp)
+    return F.fc_plan_hybrid(cu, cp)[0]
+
+
+def brute_whole_doc(F, cu, cp):
+    """Least max-workload over every whole-document placement (cp**n of
+    them; small cases only), the optimum the ILP of Sec. 3.4 would find
+    among whole-document plans."""
+    import itertools
+    n = len(cu) - 1
+    best = None
+    for assign in itertools.product(range(cp), repeat=n):
+        if assign[0] != 0:   # worker relabelling: fix document 0 on worker 0
+            continue
+        plan = np.array([[k, assign[k], 0, int(cu[k + 1] - cu[k])] for k in range(n)], dtype=np.int32)
+        w = max(F.fc_plan_stats(cu, cp, plan, 1, 1)["work"])
+        best = w if best is None else min(best, w)
+    return best
+
+
+def study_planner(args):
+    """Planner quality on synthetic lengths (a host-only analogue of the
+    paper's Table 2 without its datasets or ILP solver): imbalance max W /
+    mean W, token spread, received-KV tokens |R_r| (max over workers), the
+    Eq. 4 and Eq. 5 volumes, and the C++ planner's time per sequence; plus,
+    on small cases, each planner's max W against the best whole-document
+    placement found by brute force."""
+    from paper_2606_08476_amd import flashcp as F
+    from paper_2606_08476_amd import synth
+    rows = []
+    sweeps = [("llama8b", cp) for cp in (2, 4, 8, 16, 32)] + [("wholedoc", 8), ("longdoc", 16),
+                                                              ("hybrid70b", 32)]
+    for wl, cp in sweeps:
+        w = synth.WORKLOADS[wl]
+        acc = {p: {"imbalance": [], "tok_spread": [], "recv_max": [], "eq4": [], "eq5": [],
+                   "ms": []} for p in PLANNERS}
+        for seed in range(args.seeds):
+            cu = synth.cu_seqlens(synth.doc_lengths(wl, seed=100 + seed))
+            for pn in PLANNERS:
+                t = []
+                for _ in range(3):
+                    t0 = time.perf_counter()
+                    plan = run_planner(F, pn, cu, cp)
+                    t.append(time.perf_counter() - t0)
+                st = F.fc_plan_stats(cu, cp, plan, w.hkv, w.d)
+                a = acc[pn]
+                a["imbalance"].append(st["imbalance"])
+                a["tok_spread"].append(max(st["tokens"]) / (sum(st["tokens"]) / cp))
+                a["recv_max"].append(max(st["recv_tokens"]))
+                a["eq4"].append(st["eq4"])
+                a["eq5"].append(st["eq5"])
+                a["ms"].append(sorted(t)[1] * 1e3)
+        for pn in PLANNERS:
+            a = acc[pn]
+            row = {"study": "planner", "workload": wl, "context": w.context, "cp": cp, "planner": pn,
+                   "seeds": args.seeds,
+                   "imbalance_mean": round(float(np.mean(a["imbalance"])), 4),
+                   "imbalance_max": round(float(np.max(a["imbalance"])), 4),
+                   "max_tokens_over_mean": round(float(np.mean(a["tok_spread"])), 4),
+                   "recv_tokens_max": int(np.mean(a["recv_max"])),
+                   "eq4_elems": int(np.mean(a["eq4"])), "eq5_elems": int(np.mean(a["eq5"])),
+                   "planner_ms": round(float(np.median(a["ms"])), 3)}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+    # small cases: against the best whole-document placement
+    rng = np.random.default_rng(11)
+    small = []
+    for cp, nd in ((2, 8), (2, 10), (3, 7), (4, 7)):
+        ratios = {p: [] for p in PLANNERS}
+        for _ in range(args.seeds):
+            lens = [int(x) for x in np.exp(rng.normal(np.log(512), 1.0, size=nd)).clip(16, 8192)]
+            lens[-1] += (-sum(lens)) % cp
+            cu = synth.cu_seqlens(np.array(lens))
+            opt = brute_whole_doc(F, cu, cp)
+            for pn in PLANNERS:
+                w_max = max(F.fc_plan_stats(cu, cp, run_planner(F, pn, cu, cp), 1, 1)["work"])
+                ratios[pn].append(w_max / opt)
+        row = {"study": "planner_vs_brute_force", "cp": cp, "docs": nd, "seeds": args.seeds,
+               **{f"{p}_maxW_over_best_whole_doc": round(float(np.mean(r)), 4) for p, r in ratios.items()}}
+        small.append(row)
+        print(json.dumps(row), flush=True)
+    print("\n| lengths | N | planner | imbalance (mean / max) | max tokens / mean | max recv tokens | Eq. 4 | Eq. 5 | planner ms |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for r in rows:
+        print(f"| {r['workload']} ({r['context']}) | {r['cp']} | {r['planner']} | {r['imbalance_mean']} / "
+              f"{r['imbalance_max']} | {r['max_tokens_over_mean']} | {r['recv_tokens_max']} | "
+              f"{r['eq4_elems']:.3g} | {r['eq5_elems']:.3g} | {r['planner_ms']} |")
+    print("\n| N | docs | " + " | ".join(PLANNERS) + " |")
+    print("|---|---|" + "---|" * len(PLANNERS))
+    for r in small:
+        print(f"| {r['cp']} | {r['docs']} | " + " | ".join(
+            str(r[f'{p}_maxW_over_best_whole_doc']) for p in PLANNERS) + " |")
 
 
 def plan_for(F, w, cu):
@@ -119,8 +228,100 @@ def cpu_baseline(cu, view_tables, x, w, seconds):
                       f"rank's work, forward + backward in fp32, {dt:.1f} s"}
 
 
+def study_granularity(args):
+    """Kernel efficiency against shard granularity on one GPU (an analogue of
+    the paper's kernel-efficiency figure, Sec. 2.3): one 128K-token document
+    and 16 documents of 8K, each run unsharded (one rank holds every query)
+    and as every rank's share under Per-Doc and per-sequence (Llama3 CP)
+    plans at N = 4 and 8. Each configuration runs all of its ranks' shares
+    one after another (gather, forward partials, merge, backward) and
+    reports useful TFLOP/s over the summed time, and over N times the
+    slowest rank (the step time of an N-GPU run with a free exchange)."""
+    import torch
+    from paper_2606_08476_amd import flashcp as F
+    from paper_2606_08476_amd import synth
+    dev = torch.device("cuda:0")
+    hq, hkv, d = 32, 8, 128
+    bf, f32 = torch.bfloat16, torch.float32
+    patterns = {"1x128K": [131072], "16x8K": [8192] * 16}
+    configs = [("whole", 1), ("per_doc", 4), ("per_doc", 8), ("per_seq", 4), ("per_seq", 8)]
+    rows = []
+    g = torch.Generator(device=dev)
+    for pname, lens in patterns.items():
+        cu = synth.cu_seqlens(np.array(lens))
+        T = int(cu[-1])
+        g.manual_seed(7)
+        q_all = torch.randn(T, hq, d, device=dev, generator=g).to(bf)
+        do_all = torch.randn(T, hq, d, device=dev, generator=g).to(bf)
+        k_pk = torch.randn(T, hkv, d, device=dev, generator=g).to(bf)
+        v_pk = torch.randn(T, hkv, d, device=dev, generator=g).to(bf)
+        for kind, cp in configs:
+            plan = F.fc_plan_whole_lpt(cu, 1) if kind == "whole" else run_planner(F, kind, cu, cp)
+            per_rank = []
+            pairs_total = 0
+            for rank in range(cp):
+                v = F.View(cu, plan, cp, rank, hq, hkv, d).bind(dev)
+                i = v.info
+                tq, tr = i["t_q"], i["t_recv"]
+                pairs_total += i["pairs_loc"] + i["pairs_recv"]
+                qg = torch.from_numpy(v.export()["q_gpos"].astype(np.int64)).to(dev)
+                q, do = q_all[qg].contiguous(), do_all[qg].contiguous()
+                e = lambda *sh, dt=f32: torch.empty(*sh, dtype=dt, device=dev)
+                kl, vl = e(tq, hkv, d, dt=bf), e(tq, hkv, d, dt=bf)
+                kr, vr = e(tr, hkv, d, dt=bf), e(tr, hkv, d, dt=bf)
+                oa, ob, la, lb = e(tq, hq, d), e(tq, hq, d), e(hq, tq), e(hq, tq)
+                o, lse, delta = e(tq, hq, d, dt=bf), e(hq, tq), e(hq, tq)
+                dq, dkl, dvl = e(tq, hq, d), e(tq, hkv, d), e(tq, hkv, d)
+                dkr, dvr = e(tr, hkv, d), e(tr, hkv, d)
+                ws = torch.empty(max(v.workspace_size()[2], 1), dtype=torch.uint8, device=dev)
+                no_ws = torch.empty(1, dtype=torch.uint8, device=dev)
+
+                def run():
+                    F.fc_kv_gather(v, k_pk, v_pk, kl, vl, kr, vr)
+                    if tr:
+                        F.fc_attn_fwd_partials(v, q, kl, vl, kr, vr, 0.0, oa, la, ob, lb)
+                        F.fc_lse_merge(oa, la, ob, lb, o, None, lse)
+                    else:
+                        F.fc_attn_fwd(v, q, kl, vl, kr, vr, 0.0, F.FC_TWO_PASS, o, None, lse, no_ws)
+                    F.fc_bwd_preprocess(v, o, do, delta)
+                    F.fc_attn_bwd_pass(v, q, kl, vl, kr, vr, lse, delta, do, 0.0, dq, dkl, dvl, dkr, dvr, ws)
+
+                for _ in range(2):
+                    run()
+                torch.cuda.synchronize()
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                reps = 5
+                ev[0].record()
+                for _ in range(reps):
+                    run()
+                ev[1].record()
+                torch.cuda.synchronize()
+                per_rank.append(ev[0].elapsed_time(ev[1]) / reps)
+                v.close()
+            flops = 14.0 * d * hq * pairs_total
+            tsum, tmax = sum(per_rank), max(per_rank)
+            row = {"study": "granularity", "pattern": pname, "plan": kind, "cp": cp,
+                   "pairs_per_head": int(pairs_total),
+                   "sum_ms": round(tsum, 3), "max_rank_ms": round(tmax, 3),
+                   "tflops_sum": round(flops / (tsum * 1e-3) / 1e12, 1),
+                   "tflops_n_x_max": round(flops / (cp * tmax * 1e-3) / 1e12, 1)}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+    print("\n| documents | plan | N | pairs/head | sum over ranks ms | slowest rank ms | TFLOP/s (sum) | TFLOP/s (N x slowest) |")
+    print("|---|---|---|---|---|---|---|---|")
+    for r in rows:
+        print(f"| {r['pattern']} | {r['plan']} | {r['cp']} | {r['pairs_per_head']:.4g} | {r['sum_ms']} | "
+              f"{r['max_rank_ms']} | {r['tflops_sum']} | {r['tflops_n_x_max']} |")
+
+
 def main():
     args = parse()
+    if args.study == "planner":
+        study_planner(args)
+        return
+    if args.study == "granularity":
+        study_granularity(args)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs one rank's share on one GPU; --gpus must be 1 "
               "(multi-GPU exchange is not part of it)", file=sys.stderr)

@@ -89,6 +89,13 @@ typedef struct {
 int fc_plan_per_doc(const int32_t* cu_seqlens, int32_t n_docs, int32_t cp,
                     fc_shard* out, int64_t cap, int64_t* n_out);
 
+/* Per-sequence sharding, the Llama3 CP baseline (Sec. 2.2): the packed
+ * sequence of C = cu_seqlens[n_docs] tokens, not each document, is cut at
+ * floor(j*C/(2cp)), j = 0..2cp; chunk i goes to worker min(i, 2cp-1-i); a
+ * chunk that spans documents gives one shard per document it meets. */
+int fc_plan_per_seq(const int32_t* cu_seqlens, int32_t n_docs, int32_t cp,
+                    fc_shard* out, int64_t cap, int64_t* n_out);
+
 /* Whole documents only, longest first onto the least-loaded worker by
  * workload W (Algorithm 1, the Min_Worker_Add loop); ties go to the lower
  * document index and the lower worker index. Eq. 2 is not enforced. */

@@ -13,6 +13,9 @@ workload, because W is additive over a split of a shard).
 Readings of points the paper leaves open (each also listed in the design
 notes):
 
+* Per-sequence (the Llama3 CP baseline, Sec. 2.2): as Per-Doc, but the
+  whole packed sequence of C tokens is cut at floor(j*C/(2N)), so a chunk
+  may span documents (one shard per document it meets).
 * Per-Doc (Sec. 2.3): document k of length L is cut at
   ``c_k + floor(j*L/(2N))`` for j = 0..2N; chunk i goes to worker
   ``min(i, 2N-1-i)`` (0-indexed, so worker i gets chunks i and 2N-1-i).
@@ -90,6 +93,30 @@ def plan_per_doc(cu, cp: int) -> np.ndarray:
     rows = []
     for k, L in enumerate(_lens(cu)):
         rows += [(k, r, o, l) for r, o, l in per_doc_chunks(L, cp)]
+    return canonical(rows)
+
+
+def plan_per_seq(cu, cp: int) -> np.ndarray:
+    """The Llama3 CP baseline (Sec. 2.2): the packed sequence of C tokens,
+    not each document, is cut into 2N chunks [floor(iC/2N), floor((i+1)C/2N))
+    and chunk i goes to worker min(i, 2N-1-i). Written token by token: every
+    global position is given its chunk's worker and the runs of equal
+    (document, worker) become shards."""
+    cu = [int(x) for x in cu]
+    total = cu[-1]
+    rows = []
+    doc = 0
+    for g in range(total):
+        while g >= cu[doc + 1]:
+            doc += 1
+        i = (g * 2 * cp) // total
+        # g lies in chunk i iff floor(iC/2N) <= g < floor((i+1)C/2N)
+        while (i * total) // (2 * cp) > g:
+            i -= 1
+        while ((i + 1) * total) // (2 * cp) <= g:
+            i += 1
+        rank = i if i < cp else 2 * cp - 1 - i
+        rows.append((doc, rank, g - cu[doc], 1))
     return canonical(rows)
 
 

@@ -249,6 +249,29 @@ int fc_plan_per_doc(const int32_t* cu, int32_t n_docs, int32_t cp, fc_shard* out
   return emit(canonicalize(rows), out, cap, n_out);
 }
 
+int fc_plan_per_seq(const int32_t* cu, int32_t n_docs, int32_t cp, fc_shard* out, int64_t cap,
+                    int64_t* n_out) {
+  clear_error();
+  std::vector<int64_t> lens;
+  if (int rc = doc_lengths(cu, n_docs, lens)) return rc;
+  if (cp < 1) return fail(FC_ERR_INVALID_ARG, "cp must be >= 1");
+  // chunk i of the whole packed sequence, intersected with every document it
+  // meets (documents and chunks are both sorted, so one merge walk)
+  const int64_t total = cu[n_docs], parts = 2 * int64_t(cp);
+  std::vector<fc_shard> rows;
+  int32_t k = 0;
+  for (int64_t i = 0; i < parts; ++i) {
+    const int64_t a = i * total / parts, b = (i + 1) * total / parts;
+    const int32_t r = int32_t(i < cp ? i : parts - 1 - i);
+    while (k < n_docs && cu[k + 1] <= a) ++k;
+    for (int32_t d = k; d < n_docs && cu[d] < b; ++d) {
+      const int64_t lo = std::max<int64_t>(a, cu[d]), hi = std::min<int64_t>(b, cu[d + 1]);
+      if (hi > lo) rows.push_back({d, r, int32_t(lo - cu[d]), int32_t(hi - lo)});
+    }
+  }
+  return emit(canonicalize(rows), out, cap, n_out);
+}
+
 int fc_plan_whole_lpt(const int32_t* cu, int32_t n_docs, int32_t cp, fc_shard* out, int64_t cap,
                       int64_t* n_out) {
   clear_error();

@@ -26,7 +26,7 @@ ERRORS = {
 
 # every function the header declares
 EXPORTS = [
-    "fc_plan_per_doc", "fc_plan_whole_lpt", "fc_plan_hybrid", "fc_plan_validate",
+    "fc_plan_per_doc", "fc_plan_per_seq", "fc_plan_whole_lpt", "fc_plan_hybrid", "fc_plan_validate",
     "fc_plan_stats", "fc_view_create", "fc_view_get_info", "fc_view_export", "fc_view_bind",
     "fc_view_destroy", "fc_workspace_size", "fc_kv_gather", "fc_attn_fwd",
     "fc_attn_fwd_partial", "fc_attn_fwd_partials", "fc_lse_merge", "fc_attn_bwd", "fc_bwd_preprocess",
@@ -74,6 +74,7 @@ def lib():
         L = C.CDLL(_LIB_PATH)
         sig = {
             "fc_plan_per_doc": [I32P, C.c_int32, C.c_int32, C.POINTER(Shard), C.c_int64, C.POINTER(C.c_int64)],
+            "fc_plan_per_seq": [I32P, C.c_int32, C.c_int32, C.POINTER(Shard), C.c_int64, C.POINTER(C.c_int64)],
             "fc_plan_whole_lpt": [I32P, C.c_int32, C.c_int32, C.POINTER(Shard), C.c_int64, C.POINTER(C.c_int64)],
             "fc_plan_hybrid": [I32P, C.c_int32, C.c_int32, C.c_double, C.POINTER(Shard), C.c_int64,
                                C.POINTER(C.c_int64), C.POINTER(C.c_uint8)],
@@ -147,6 +148,11 @@ def _plan_out(fn, *args):
 def fc_plan_per_doc(cu, cp: int) -> np.ndarray:
     a, p, n = _cu(cu)
     return _plan_out(lib().fc_plan_per_doc, p, n, cp)
+
+
+def fc_plan_per_seq(cu, cp: int) -> np.ndarray:
+    a, p, n = _cu(cu)
+    return _plan_out(lib().fc_plan_per_seq, p, n, cp)
 
 
 def fc_plan_whole_lpt(cu, cp: int) -> np.ndarray:

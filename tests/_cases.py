@@ -28,15 +28,18 @@ class Case:
 
 
 def make_case(name, workload, context=None, cp=None, rank=None, hq=None, hkv=None, d=None,
-              seed=None, lens=None) -> Case:
+              seed=None, lens=None, plan=None) -> Case:
     w = synth.WORKLOADS[workload]
     cp = w.cp if cp is None else cp
     if lens is None:
         lens = synth.doc_lengths(workload, context=context, seed=seed)
     cu = synth.cu_seqlens(lens)
-    if w.plan == "per_doc":
+    kind = w.plan if plan is None else plan
+    if kind == "per_seq":
+        plan = OP.plan_per_seq(cu, cp)
+    elif kind == "per_doc":
         plan = OP.plan_per_doc(cu, cp)
-    elif w.plan == "whole_lpt":
+    elif kind == "whole_lpt":
         plan = OP.plan_whole_lpt(cu, cp)
     else:
         plan = OP.plan_hybrid(cu, cp)[0]
@@ -79,6 +82,9 @@ SMALL = {
     "wholedoc_16k": dict(workload="wholedoc", context=16384),
     "longdoc_16k": dict(workload="longdoc", context=16384),
     "hybrid70b_16k": dict(workload="hybrid70b", context=16384),
+    # the Llama3 CP baseline plan (chunks of the whole sequence) through the
+    # same kernels
+    "llama8b_8k_per_seq": dict(workload="llama8b", context=8192, plan="per_seq"),
     # other grouped-query shapes through the same kernels
     "llama8b_8k_g2": dict(workload="llama8b", context=8192, hq=16, hkv=8),
     "llama8b_8k_g1": dict(workload="llama8b", context=8192, hq=8, hkv=8, rank=5),

@@ -60,3 +60,20 @@ def test_committed_records_parse():
             assert os.path.exists(os.path.join(ROOT, src)), src
         v = bench.measured_traffic(rec["entry"], rec["workload"])
         assert v is None or v == rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
+
+
+def test_planner_study_runs_on_the_host():
+    """`bench.py --study planner` needs no GPU: one JSON line per (lengths,
+    N, planner), the Llama3 per-sequence plan is the most imbalanced on the
+    log-normal lengths and the hybrid meets its target ratio."""
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--study", "planner",
+                        "--seeds", "1"], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    rows = [json.loads(x) for x in r.stdout.splitlines() if x.startswith("{")]
+    plan_rows = [x for x in rows if x["study"] == "planner"]
+    assert len(plan_rows) == 8 * len(bench.PLANNERS)
+    for cp in (2, 4, 8, 16, 32):
+        by = {x["planner"]: x for x in plan_rows if x["workload"] == "llama8b" and x["cp"] == cp}
+        assert by["per_seq"]["imbalance_max"] > by["per_doc"]["imbalance_max"]
+        assert by["hybrid"]["imbalance_max"] <= 1.05 + 1e-12
+        assert by["whole_lpt"]["recv_tokens_max"] == 0

@@ -57,6 +57,7 @@ def _random_cases(n=25, seed=7):
 def test_planners_bit_exact_random():
     for cu, N in _random_cases():
         assert np.array_equal(F.fc_plan_per_doc(cu, N), P.plan_per_doc(cu, N))
+        assert np.array_equal(F.fc_plan_per_seq(cu, N), P.plan_per_seq(cu, N))
         assert np.array_equal(F.fc_plan_whole_lpt(cu, N), P.plan_whole_lpt(cu, N))
         for R in (1.0, 1.05, 1.3):
             a, ia = F.fc_plan_hybrid(cu, N, R)
@@ -70,11 +71,12 @@ def test_planners_bit_exact_workloads(name):
     w = synth.WORKLOADS[name]
     cu = synth.cu_seqlens(synth.doc_lengths(name))
     assert np.array_equal(F.fc_plan_per_doc(cu, w.cp), P.plan_per_doc(cu, w.cp))
+    assert np.array_equal(F.fc_plan_per_seq(cu, w.cp), P.plan_per_seq(cu, w.cp))
     assert np.array_equal(F.fc_plan_whole_lpt(cu, w.cp), P.plan_whole_lpt(cu, w.cp))
     a, ia = F.fc_plan_hybrid(cu, w.cp)
     b, ib = P.plan_hybrid(cu, w.cp)
     assert np.array_equal(a, b) and np.array_equal(ia, ib)
-    for plan in (a, F.fc_plan_per_doc(cu, w.cp), F.fc_plan_whole_lpt(cu, w.cp)):
+    for plan in (a, F.fc_plan_per_doc(cu, w.cp), F.fc_plan_per_seq(cu, w.cp), F.fc_plan_whole_lpt(cu, w.cp)):
         assert F.fc_plan_stats(cu, w.cp, plan, w.hkv, w.d) == P.stats(cu, w.cp, plan, w.hkv, w.d)
 
 

@@ -188,3 +188,47 @@ def test_eq4_eq5_and_receive_sets():
     for j in range(8):
         want = sum((16 - j) * ci - 2 * ci for ci in c)
         assert st["recv_tokens"][j] == want
+
+
+def test_per_seq_hand_example():
+    """Llama3 CP (Sec. 2.2) on documents [0,5), [5,12), [12,30), N = 2: the
+    sequence is cut into [0,7), [7,15), [15,22), [22,30), going to workers
+    0, 1, 1, 0. Document 1 is split at token 7 (offset 2); document 2's
+    tokens 12..21 (chunks 1 and 2) stay together on worker 1 and 22..29 go to
+    worker 0 (offset 10)."""
+    plan = P.plan_per_seq(_cu([5, 7, 18]), 2)
+    assert plan.tolist() == [[0, 0, 0, 5], [1, 0, 0, 2], [1, 1, 2, 5], [2, 1, 0, 10], [2, 0, 10, 8]]
+
+
+def test_per_seq_of_one_document_is_per_doc():
+    """With a single document the sequence cut and the document cut coincide."""
+    for L in (1, 7, 64, 1000, 4099):
+        for N in (1, 2, 3, 8):
+            assert np.array_equal(P.plan_per_seq(_cu([L]), N), P.plan_per_doc(_cu([L]), N))
+
+
+def test_per_seq_tokens_and_intervals():
+    """Worker r holds exactly chunks r and 2N-1-r of the whole sequence: its
+    token count is the closed form, and the oracle (token by token) equals
+    an interval-intersection construction of the same rule."""
+    rng = np.random.default_rng(7)
+    for _ in range(40):
+        N = int(rng.choice([1, 2, 3, 4, 8]))
+        lens = [int(x) for x in rng.integers(1, 300, size=int(rng.integers(1, 9)))]
+        cu = _cu(lens)
+        T = int(cu[-1])
+        plan = P.plan_per_seq(cu, N)
+        P.validate(cu, N, plan)
+        tok = [0] * N
+        for _, r, _, l in plan:
+            tok[r] += int(l)
+        b = [(i * T) // (2 * N) for i in range(2 * N + 1)]
+        assert tok == [(b[r + 1] - b[r]) + (b[2 * N - r] - b[2 * N - 1 - r]) for r in range(N)]
+        rows = []
+        for i in range(2 * N):
+            r = i if i < N else 2 * N - 1 - i
+            for k in range(len(lens)):
+                lo, hi = max(b[i], int(cu[k])), min(b[i + 1], int(cu[k + 1]))
+                if hi > lo:
+                    rows.append((k, r, lo - int(cu[k]), hi - lo))
+        assert np.array_equal(plan, P.canonical(rows))
