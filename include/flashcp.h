@@ -194,7 +194,10 @@ int fc_workspace_size(fc_view view, int32_t mode, size_t* fwd_bytes, size_t* bwd
 
 /* The simulated receive (Sec. 3.2; the "data copy" cost of Sec. 4.3): from
  * packed k,v [t_packed, Hkv, d] (bf16, device) gather the rank's own rows
- * into k_loc/v_loc and its receive set, compacted, into k_recv/v_recv. */
+ * into k_loc/v_loc and its receive set, compacted, into k_recv/v_recv.
+ * Either part may be skipped by passing NULL for both of its outputs (the
+ * two parts can then run on different streams, the receive overlapping the
+ * local pass as in Sec. 3.2); at least one part must be given. */
 int fc_kv_gather(fc_view view, const void* k_packed, const void* v_packed, int64_t t_packed,
                  void* k_loc, void* v_loc, void* k_recv, void* v_recv, void* stream);
 

@@ -174,13 +174,16 @@ int fc_kv_gather(fc_view view, const void* k_packed, const void* v_packed, int64
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() + v->t_recv() == 0) return FC_OK;
-  if (!k_packed || !v_packed || (v->t_q() && (!k_loc || !v_loc)) ||
-      (v->t_recv() && (!k_recv || !v_recv)))
+  // a part whose two outputs are both NULL is skipped
+  const bool loc = k_loc || v_loc, rcv = k_recv || v_recv;
+  if (!k_packed || !v_packed || (loc && (!k_loc || !v_loc)) || (rcv && (!k_recv || !v_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  if (!loc && !rcv) return fail(FC_ERR_INVALID_ARG, "nothing to gather: every output is null");
+  const int64_t r0 = loc ? 0 : v->t_q(), r1 = rcv ? v->t_q() + v->t_recv() : v->t_q();
   // every gathered position must lie inside the packed tensors
   int64_t max_pos = -1;
-  if (v->t_q()) max_pos = std::max<int64_t>(max_pos, v->q_gpos.back());
-  if (v->t_recv()) max_pos = std::max<int64_t>(max_pos, v->recv_gpos.back());
+  if (loc && v->t_q()) max_pos = std::max<int64_t>(max_pos, v->q_gpos.back());
+  if (rcv && v->t_recv()) max_pos = std::max<int64_t>(max_pos, v->recv_gpos.back());
   if (max_pos >= t_packed)
     return fail(FC_ERR_SHAPE, "packed K/V have " + std::to_string(t_packed) +
                                   " rows, the view reads row " + std::to_string(max_pos));
@@ -188,7 +191,7 @@ int fc_kv_gather(fc_view view, const void* k_packed, const void* v_packed, int64
   return hip_status(
       fck::launch_kv_gather(static_cast<const uint16_t*>(k_packed),
                             static_cast<const uint16_t*>(v_packed), m + v->off.q_gpos,
-                            m + v->off.recv_gpos, v->t_q(), v->t_recv(), v->hkv * v->d,
+                            m + v->off.recv_gpos, v->t_q(), v->t_recv(), r0, r1, v->hkv * v->d,
                             static_cast<uint16_t*>(k_loc), static_cast<uint16_t*>(v_loc),
                             static_cast<uint16_t*>(k_recv), static_cast<uint16_t*>(v_recv),
                             reinterpret_cast<hipStream_t>(stream)),

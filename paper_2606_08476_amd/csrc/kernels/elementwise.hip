@@ -8,18 +8,19 @@
 namespace fck {
 
 // Row copies: output row i of K/V local (i < t_q) or received (i >= t_q)
-// comes from packed row q_gpos[i] or recv_gpos[i - t_q].
+// comes from packed row q_gpos[i] or recv_gpos[i - t_q]; rows r0 .. r1-1
+// of that concatenation are copied.
 __global__ __launch_bounds__(256) void kv_gather_kernel(const uint4* __restrict__ k,
                                                         const uint4* __restrict__ v,
                                                         const int32_t* __restrict__ q_gpos,
                                                         const int32_t* __restrict__ recv_gpos,
-                                                        int32_t t_q, int32_t t_r, int32_t chunks,
-                                                        uint4* k_loc, uint4* v_loc, uint4* k_recv,
-                                                        uint4* v_recv) {
-  const int64_t total = int64_t(t_q + t_r) * chunks;
+                                                        int32_t t_q, int64_t r0, int64_t r1,
+                                                        int32_t chunks, uint4* k_loc, uint4* v_loc,
+                                                        uint4* k_recv, uint4* v_recv) {
+  const int64_t total = (r1 - r0) * chunks;
   for (int64_t c = int64_t(blockIdx.x) * 256 + threadIdx.x; c < total;
        c += int64_t(gridDim.x) * 256) {
-    const int32_t row = int32_t(c / chunks), cc = int32_t(c % chunks);
+    const int32_t row = int32_t(r0 + c / chunks), cc = int32_t(c % chunks);
     const bool loc = row < t_q;
     const int64_t src = int64_t(loc ? q_gpos[row] : recv_gpos[row - t_q]) * chunks + cc;
     const int64_t dst = int64_t(loc ? row : row - t_q) * chunks + cc;
@@ -130,17 +131,18 @@ static unsigned grid_for(int64_t threads) {
 }
 
 hipError_t launch_kv_gather(const uint16_t* k, const uint16_t* v, const int32_t* q_gpos,
-                            const int32_t* recv_gpos, int32_t t_q, int32_t t_r, int32_t row_elems,
-                            uint16_t* k_loc, uint16_t* v_loc, uint16_t* k_recv, uint16_t* v_recv,
-                            hipStream_t s) {
+                            const int32_t* recv_gpos, int32_t t_q, int32_t t_r, int64_t r0,
+                            int64_t r1, int32_t row_elems, uint16_t* k_loc, uint16_t* v_loc,
+                            uint16_t* k_recv, uint16_t* v_recv, hipStream_t s) {
   const int32_t chunks = row_elems / 8;
-  const int64_t total = int64_t(t_q + t_r) * chunks;
+  if (r0 < 0 || r1 > int64_t(t_q) + t_r || r0 > r1) return hipErrorInvalidValue;
+  const int64_t total = (r1 - r0) * chunks;
   if (total == 0) return hipSuccess;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 256 * 64) blocks = 256 * 64;
   hipLaunchKernelGGL(kv_gather_kernel, dim3(unsigned(blocks)), dim3(256), 0, s,
                      reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v), q_gpos,
-                     recv_gpos, t_q, t_r, chunks, reinterpret_cast<uint4*>(k_loc),
+                     recv_gpos, t_q, r0, r1, chunks, reinterpret_cast<uint4*>(k_loc),
                      reinterpret_cast<uint4*>(v_loc), reinterpret_cast<uint4*>(k_recv),
                      reinterpret_cast<uint4*>(v_recv));
   return hipGetLastError();

@@ -87,8 +87,11 @@ hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float*
 hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o_b,
                             const float* lse_b, int32_t t, int32_t h, int32_t d, uint16_t* o_bf16,
                             float* o_f32, float* lse_out, hipStream_t s);
+// rows r0 .. r1-1 of the concatenation (local rows 0 .. t_q-1, then the
+// receive set)
 hipError_t launch_kv_gather(const uint16_t* k, const uint16_t* v, const int32_t* q_gpos,
-                            const int32_t* recv_gpos, int32_t t_q, int32_t t_r, int32_t row_elems,
+                            const int32_t* recv_gpos, int32_t t_q, int32_t t_r, int64_t r0,
+                            int64_t r1, int32_t row_elems,
                             uint16_t* k_loc, uint16_t* v_loc, uint16_t* k_recv, uint16_t* v_recv,
                             hipStream_t s);
 

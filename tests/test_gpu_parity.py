@@ -121,6 +121,26 @@ def test_gather_is_exact(key, dev):
     assert torch.equal(r.k_recv.cpu(), r.x["k_recv"]) and torch.equal(r.v_recv.cpu(), r.x["v_recv"])
 
 
+def test_gather_parts(dev):
+    """The rank's own rows and its receive set gathered by separate calls
+    (NULL outputs skip a part) equal the one-call gather bit for bit; half a
+    NULL pair, or no part at all, is rejected before any launch."""
+    r = get_run("llama8b_8k", dev)
+    x = {k: t.to(dev) for k, t in r.x.items() if k in ("k_pk", "v_pk")}
+    kl, vl = torch.empty_like(r.k_loc), torch.empty_like(r.v_loc)
+    kr, vr = torch.empty_like(r.k_recv), torch.empty_like(r.v_recv)
+    F.fc_kv_gather(r.v, x["k_pk"], x["v_pk"], None, None, kr, vr)
+    F.fc_kv_gather(r.v, x["k_pk"], x["v_pk"], kl, vl, None, None)
+    torch.cuda.synchronize()
+    for a, b in ((kl, r.k_loc), (vl, r.v_loc), (kr, r.k_recv), (vr, r.v_recv)):
+        assert torch.equal(a, b)
+    lib = F.lib()
+    T = x["k_pk"].shape[0]
+    kp, vp = x["k_pk"].data_ptr(), x["v_pk"].data_ptr()
+    assert lib.fc_kv_gather(r.v.handle, kp, vp, T, kl.data_ptr(), None, None, None, None) == -1
+    assert lib.fc_kv_gather(r.v.handle, kp, vp, T, None, None, None, None, None) == -1
+
+
 @pytest.mark.parametrize("key", SMALL)
 def test_forward_two_pass(key, dev):
     r = get_run(key, dev)

@@ -235,3 +235,4 @@ def test_backward_launch_split_covers_the_map():
         if name == "wholedoc":
             assert slots > 0
         v.close()
+
