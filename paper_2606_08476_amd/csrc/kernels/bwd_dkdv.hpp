@@ -127,13 +127,11 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   // scheduling barrier after each slot keeps this order.
   constexpr int NS = 2 * KS + 4 * DB;       // slots per step
   constexpr int EP = 16 / KS, ES = 8 / DB;  // P / dS elements per slot
-  auto step = [&](int i_, auto bufc) {
+  // The compute of one query tile; P is masked (a branch after its last
+  // slot) only on edge tiles.
+  auto tile = [&](int t0, auto bufc, bool edge) {
     constexpr int B = decltype(bufc)::value;
     constexpr uint32_t QO = B ? OQ1 : OQ0, OO = B ? OO1 : OO0, SO = 768u * B;
-    const int t0 = q0 + (i_ % ntile) * BM;
-    if (i_ + 1 < n_it) fetch(i_ + 1, B ^ 1);
-    pr = opaque(pr);
-    pt = opaque(pt);
     // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
     // (register 4g + j): rows cq < hiq exist; on a local diagonal the key is
     // seen by rows cq >= lo; on a received diagonal by rows whose receive
@@ -166,19 +164,16 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
     };
     rd(0);
     rd(1);
-#pragma unroll
-    for (int n = 0; n < NS; ++n) {
+    static_for<0, NS>([&](auto nc) {
+      constexpr int n = decltype(nc)::value;
       if (n + 2 < NS) rd(n + 2);
-      if (n == KS - 2) {  // LSE, delta and limits of the 16 rows
+      // LSE and delta of rows 8g + 4*half + 0..3, read two slots before the
+      // first slot that uses them
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+      for (int g = 0; g < 4; ++g) {
+        if (KS + 4 * g / EP == n + 2)
           l4[g] = *reinterpret_cast<const f32x4*>(smem + SO + 4 * (8 * g + 4 * half));
-          m4[g] = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
-        }
-      }
-      if (n == KS - 1) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
+        if (2 * KS + 4 * g / ES == n + 2)
           d4[g] = *reinterpret_cast<const f32x4*>(smem + SO + 256 + 4 * (8 * g + 4 * half));
       }
       const bf16x8& a = ra[n % 3];
@@ -188,13 +183,25 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
         dpacc = mfma32(a, vreg[n - KS], dpacc);
 #pragma unroll
         for (int e = (n - KS) * EP; e < (n - KS + 1) * EP; ++e) {
-          const int g = e >> 2, j = e & 3, cq = 8 * g + j;
-          const int lim = j == 0 ? m4[g].x : j == 1 ? m4[g].y : j == 2 ? m4[g].z : m4[g].w;
-          const float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], sl2, -l4[g][j] * kLog2e));
-          sacc[e] = ((cq >= lo) & (cq < hiq) & (kl < lim)) ? pij : 0.f;
+          const int g = e >> 2, j = e & 3;
+          sacc[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], sl2, -l4[g][j] * kLog2e));
         }
         if ((n - KS + 1) * EP == 8) pa[0] = pack8(sacc, 0);
-        if ((n - KS + 1) * EP == 16) pa[1] = pack8(sacc, 8);
+        if (n == 2 * KS - 1) {
+          if (edge) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+              m4[g] = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int g = e >> 2, j = e & 3, cq = 8 * g + j;
+              const int lim = j == 0 ? m4[g].x : j == 1 ? m4[g].y : j == 2 ? m4[g].z : m4[g].w;
+              sacc[e] = ((cq >= lo) & (cq < hiq) & (kl < lim)) ? sacc[e] : 0.f;
+            }
+            pa[0] = pack8(sacc, 0);
+          }
+          pa[1] = pack8(sacc, 8);
+        }
       } else if (n < 2 * KS + 2 * DB) {
         const int u = n - 2 * KS, kh = u / DB, db = u % DB;
         dv[db] = mfma32(pa[kh], a, dv[db]);
@@ -208,7 +215,25 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
         dk[db] = mfma32(sa[kh], a, dk[db]);
       }
       __builtin_amdgcn_sched_barrier(0);
-    }
+    });
+  };
+  // One pipelined iteration: start the next tile's copies, compute this one,
+  // wait for the copies. Each wave picks its own variant of the compute:
+  // unmasked where every row of the tile sees all of the wave's 32 keys
+  // (past the diagonal, a whole tile of rows, all keys in range); skipped
+  // where no row sees any of them (local keys after the tile's last row,
+  // received keys at or past every row's receive limit -- the limits do not
+  // decrease along a segment, so the last row's is the largest -- and keys
+  // past the range); masked otherwise.
+  auto step = [&](int i_, auto bufc) {
+    const int t0 = q0 + (i_ % ntile) * BM;
+    if (i_ + 1 < n_it) fetch(i_ + 1, decltype(bufc)::value ^ 1);
+    pr = opaque(pr);
+    pt = opaque(pt);
+    const int kw = k0 + 32 * wave;
+    const int tlast = min(t0 + BM, q1) - 1;
+    if (!(kw >= k1 || (src ? p.lim[tlast] <= kw : tlast < kw)))
+      tile(t0, bufc, !(t0 >= qfull && t0 + BM <= q1 && kw + 32 <= k1));
     wait_async();
     __syncthreads();
   };

@@ -128,9 +128,11 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
     }
     // key k0 + 4*half + c (c = 32*mb + 8*(i/4) + i%4 for register i) is seen
     // iff c < rel: keys past the range, and later keys on diagonal tiles,
-    // give P = 0
+    // give P = 0. Only edge tiles (diagonal, or running past the range)
+    // mask, in one branch before each half's dS.
     const bool diag = !rs && k0 >= ldiag;
     const int rel = (diag ? min(hi, qrow + 1) : hi) - k0 - 4 * half;
+    const bool edge = diag || k0 + BN > hi;
 
     f32x16 s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
     bf16x8 ring[3], sb[4];
@@ -146,14 +148,20 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
       }
     };
     auto pexp = [&](int mb, int i) {
-      const float pij = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], sl2, -lse2));
-      s[mb][i] = 32 * mb + 8 * (i >> 2) + (i & 3) < rel ? pij : 0.f;
+      s[mb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], sl2, -lse2));
+    };
+    auto mask = [&](int mb) {
+      if (edge) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          s[mb][i] = 32 * mb + 8 * (i >> 2) + (i & 3) < rel ? s[mb][i] : 0.f;
+      }
     };
     auto dsv = [&](int mb, int i) { dp[mb][i] = s[mb][i] * (dp[mb][i] - del); };
     rd(0);
     rd(1);
-#pragma unroll
-    for (int n = 0; n < NS; ++n) {
+    static_for<0, NS>([&](auto nc) {
+      constexpr int n = decltype(nc)::value;
       if (n + 2 < NS) rd(n + 2);
       const bf16x8& a = ring[n % 3];
       if (n < 2 * KS) {
@@ -165,6 +173,7 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
       } else if (n < 4 * KS) {
         const int ks = n % KS, mb = (n - 2 * KS) / KS;
         dp[mb] = mfma32(a, oreg[ks], dp[mb]);
+        if (mb == 1 && ks == 0) mask(0);
         if (mb == 0) {
 #pragma unroll
           for (int e = ks * EP; e < (ks + 1) * EP; ++e) pexp(1, e);
@@ -177,6 +186,7 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
       } else {
         const int u = n - 4 * KS, kk = u / DB, db = u % DB;
         dq[db] = mfma32(a, sb[kk], dq[db]);
+        if (u == 0) mask(1);
         if (u < 2 * DB) {
 #pragma unroll
           for (int e = u * EQ; e < (u + 1) * EQ; ++e) dsv(1, e);
@@ -185,7 +195,7 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
         }
       }
       __builtin_amdgcn_sched_barrier(0);
-    }
+    });
     wait_async();
     __syncthreads();
   };

@@ -21,6 +21,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace fck {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -214,6 +216,17 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 }
 
 // Index of this thread's wave in the workgroup, as a wave-uniform value.
+// Calls f(std::integral_constant<int, I>()) for I = B .. E-1: a fully
+// unrolled loop whose index is a compile-time constant, whatever the size of
+// the body (a plain unroll pragma gives up past the unroller's size limit).
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>());
+    static_for<B + 1, E>(f);
+  }
+}
+
 __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
