@@ -70,20 +70,20 @@ fck::FwdParams fwd_params(const View& v, const int32_t* items, const int32_t* pe
   return p;
 }
 
-// Both partial passes of the two-pass forward in one launch: the received
-// items write (o_recv, lse_recv), the local items (o_loc, lse_loc).
+// Both partial passes of the two-pass forward in one launch over the fused
+// items: each workgroup runs its query tile's received range, writes that
+// partial (o_recv, lse_recv), then runs the local range (o_loc, lse_loc).
 int launch_partials(const View& v, const void* q, const void* k_loc, const void* v_loc,
                     const void* k_recv, const void* v_recv, float scale, float* o_loc,
                     float* lse_loc, float* o_recv, float* lse_recv, hipStream_t s) {
   const int32_t* m = v.dev_meta;
-  fck::FwdParams p = fwd_params(v, m + v.off.fwd_two, m + v.off.perm_fwd_two,
-                                int64_t(v.fwd_two.size() / 8), q, k_loc, v_loc, k_recv, v_recv,
+  fck::FwdParams p = fwd_params(v, m + v.off.fwd_fused, m + v.off.perm_fwd_fused,
+                                int64_t(v.fwd_fused.size() / 8), q, k_loc, v_loc, k_recv, v_recv,
                                 scale);
   p.o_f32 = o_loc;
   p.lse = lse_loc;
-  p.n_first = int32_t(v.fwd_recv.size() / 8);
-  p.o_f32_first = o_recv;
-  p.lse_first = lse_recv;
+  p.o_f32_recv = o_recv;
+  p.lse_recv = lse_recv;
   return hip_status(fck::launch_fwd(p, v.d, v.heads_per_tile, false, s), "attn_fwd launch");
 }
 

@@ -116,9 +116,6 @@ void View::build_tiles() {
   perm_fwd_local = lpt_order(fwd_cost(fwd_local));
   perm_fwd_recv = lpt_order(fwd_cost(fwd_recv));
   perm_fwd_fused = lpt_order(fwd_cost(fwd_fused));
-  fwd_two = fwd_recv;
-  fwd_two.insert(fwd_two.end(), fwd_local.begin(), fwd_local.end());
-  perm_fwd_two = lpt_order(fwd_cost(fwd_two));
   std::vector<int64_t> bc(bwd.size() / 8);
   for (size_t i = 0; i < bc.size(); ++i) bc[i] = ceil_div(bwd[8 * i + 3] - bwd[8 * i + 2], bm_bwd);
   perm_bwd = lpt_order(bc);
@@ -189,8 +186,6 @@ void View::build_meta() {
   off.bwd_launch = put(bwd_launch);
   off.perm_bwd_launch = put(perm_bwd_launch);
   off.bwd_reduce = put(bwd_reduce);
-  off.fwd_two = put(fwd_two);
-  off.perm_fwd_two = put(perm_fwd_two);
   if (meta.empty()) meta.resize(64, 0);
 }
 

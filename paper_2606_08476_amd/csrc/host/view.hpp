@@ -21,9 +21,6 @@ struct View {
   // work lists, 8 int32 per item (layout documented in flashcp.h)
   std::vector<int32_t> fwd_local, fwd_recv, fwd_fused, bwd;
   std::vector<int32_t> perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
-  // both partial passes in one launch: the received items, then the local
-  // items (item index < n_fwd_recv selects the received outputs)
-  std::vector<int32_t> fwd_two, perm_fwd_two;
   // backward launch list: the key-major items with long query ranges split
   // into parts that write partial dK/dV (last field: partial slot, -1 for a
   // direct write), and one reduce entry per split key tile
@@ -37,7 +34,6 @@ struct View {
   struct {
     int64_t fwd_local, fwd_recv, fwd_fused, bwd;
     int64_t perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
-    int64_t fwd_two, perm_fwd_two;
     int64_t q_gpos, recv_gpos, lim;
     int64_t bwd_launch, perm_bwd_launch, bwd_reduce;
   } off{};

@@ -11,14 +11,20 @@
 // computed:
 //   S^T = K Q^T        MFMA 32x32x16, Q held in registers (B operand), so a
 //                      query is a lane and its row statistics are per lane;
-//   online softmax     base 2, scale folded into one FMA per score; the
-//                      output is rescaled only when a row maximum grows by
+//   online softmax     base 2, scale folded into one FMA per score; a row's
+//                      output is rescaled only when its maximum grows by
 //                      more than 2^8 (the result is the same: numerator and
-//                      denominator share the stale maximum);
+//                      denominator share the stale maximum). The decision is
+//                      per row, so a row's arithmetic does not depend on the
+//                      other rows of its tile (any query tiling gives the
+//                      same bits);
 //   O^T += V^T P^T     V^T read from LDS with transpose reads, P^T straight
 //                      from the S^T accumulator registers.
-// Output: the final O (bf16, optionally fp32) and LSE, or an fp32 partial
-// O/LSE for the log-sum-exp merge.
+// Output (template OUT): the final O (bf16, optionally fp32) and LSE; or an
+// fp32 partial O/LSE for the log-sum-exp merge; or, for items that carry a
+// received and a local range, both partials: the received range is run
+// first and its partial written when the local range starts, so the query
+// tile is loaded once and the tile pipeline runs on across the switch.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -26,8 +32,11 @@
 
 namespace fck {
 
-template <int D, int HPW, bool FINAL>
+enum { kOutPartial = 0, kOutFinal = 1, kOutPaired = 2 };
+
+template <int D, int HPW, int OUT>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
+  constexpr bool FINAL = OUT == kOutFinal, PAIRED = OUT == kOutPaired;
   constexpr int BN = 64;        // keys per tile
   constexpr int WPH = 4 / HPW;  // waves per query head
   constexpr int KS = D / 16;    // MFMA k-steps over the head dim
@@ -46,8 +55,6 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int hc = rest % p.head_chunks;
   const int item = p.perm[rest / p.head_chunks];
   const int32_t* it = p.items + 8 * item;
-  float* const o_part = item < p.n_first ? p.o_f32_first : p.o_f32;
-  float* const lse_out = item < p.n_first ? p.lse_first : p.lse;
   const int q0 = it[0], q1 = it[1], r0 = it[2], r1 = it[3], l0 = it[4], l1 = it[5];
   const int ldiag = it[6];
 
@@ -102,6 +109,44 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   for (int db = 0; db < DB; ++db) oacc[db] = zero16();
   float m = -INFINITY;  // reference row maximum (scaled, log2 units)
   float lsum = 0.f;     // this lane's share of the row sum
+
+  // normalised O and the LSE of the keys seen so far, to o_out/lse_out
+  // (final: bf16 O, plus fp32 O when o_out is non-null)
+  auto write_out = [&](float* o_out, float* lse_out) {
+    const float tot = lsum + __shfl_xor(lsum, 32);
+    const float inv = tot > 0.f ? 1.f / tot : 0.f;
+    const float lse = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
+    if (qvalid) {
+      const size_t ob = ((size_t)qrow * p.hq + h) * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int dcol = 32 * db + 8 * g + 4 * half;
+          f32x4 v;
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) v[jj] = oacc[db][4 * g + jj] * inv;
+          if (FINAL) {
+            uint2 packed;
+            packed.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
+            packed.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
+            *reinterpret_cast<uint2*>(p.o_bf16 + ob + dcol) = packed;
+          }
+          if (!FINAL || o_out) *reinterpret_cast<f32x4*>(o_out + ob + dcol) = v;
+        }
+      }
+      if (half == 0) lse_out[(size_t)h * p.t_q + qrow] = lse;
+    }
+  };
+  // paired items: the received partial is complete when the local range
+  // starts; write it and start the local one from empty
+  auto switch_source = [&]() {
+    write_out(p.o_f32_recv, p.lse_recv);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) oacc[db] = zero16();
+    m = -INFINITY;
+    lsum = 0.f;
+  };
   wait_async();
   __syncthreads();
 
@@ -111,6 +156,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
+    if (PAIRED && j == n_r) switch_source();
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) pk[ks] = opaque(pk[ks]);
 #pragma unroll
@@ -144,10 +190,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[mb][i]);
     mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
-    if (__any(mx > m + kLazy)) {
-      const float mnew = fmaxf(m, mx);
-      const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mnew);
-      m = mnew;
+    const bool grow = mx > m + kLazy;  // implies mx > m
+    if (__any(grow)) {
+      // rows that do not grow keep their maximum and scale by exactly 1
+      const float alpha =
+          !grow ? 1.f : m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mx);
+      m = grow ? mx : m;
       lsum *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
@@ -186,48 +234,28 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     if (j + 1 < n_t) step(j + 1, std::integral_constant<int, 1>());
   }
 
-  lsum += __shfl_xor(lsum, 32);
-  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-  const float lse = lsum > 0.f ? (m + __log2f(lsum)) * kLn2 : -INFINITY;
-  if (qvalid) {
-    const size_t ob = ((size_t)qrow * p.hq + h) * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int dcol = 32 * db + 8 * g + 4 * half;
-        f32x4 v;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) v[jj] = oacc[db][4 * g + jj] * inv;
-        if (FINAL) {
-          uint2 packed;
-          packed.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
-          packed.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
-          *reinterpret_cast<uint2*>(p.o_bf16 + ob + dcol) = packed;
-        }
-        if (!FINAL || o_part) *reinterpret_cast<f32x4*>(o_part + ob + dcol) = v;
-      }
-    }
-    if (half == 0) lse_out[(size_t)h * p.t_q + qrow] = lse;
-  }
+  if (PAIRED && n_r == n_t) switch_source();  // no local tile (never empty in practice)
+  write_out(p.o_f32, p.lse);
 }
 
 template <int D, int HPW>
-static hipError_t launch_fwd_t(const FwdParams& p, bool final_out, hipStream_t s) {
+static hipError_t launch_fwd_t(const FwdParams& p, int out, hipStream_t s) {
   const dim3 grid(unsigned(p.n_items) * p.hkv * p.head_chunks), block(256);
-  if (final_out)
-    hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, true>), grid, block, 0, s, p);
+  if (out == kOutFinal)
+    hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, kOutFinal>), grid, block, 0, s, p);
+  else if (out == kOutPaired)
+    hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, kOutPaired>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, kOutPartial>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 
 template <int D>
-static hipError_t launch_fwd_d(const FwdParams& p, int hpw, bool final_out, hipStream_t s) {
+static hipError_t launch_fwd_d(const FwdParams& p, int hpw, int out, hipStream_t s) {
   switch (hpw) {
-    case 1: return launch_fwd_t<D, 1>(p, final_out, s);
-    case 2: return launch_fwd_t<D, 2>(p, final_out, s);
-    case 4: return launch_fwd_t<D, 4>(p, final_out, s);
+    case 1: return launch_fwd_t<D, 1>(p, out, s);
+    case 2: return launch_fwd_t<D, 2>(p, out, s);
+    case 4: return launch_fwd_t<D, 4>(p, out, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -235,8 +263,9 @@ static hipError_t launch_fwd_d(const FwdParams& p, int hpw, bool final_out, hipS
 hipError_t launch_fwd(const FwdParams& p, int d, int heads_per_tile, bool final_out,
                       hipStream_t s) {
   if (p.n_items == 0) return hipSuccess;
-  if (d == 64) return launch_fwd_d<64>(p, heads_per_tile, final_out, s);
-  if (d == 128) return launch_fwd_d<128>(p, heads_per_tile, final_out, s);
+  const int out = final_out ? kOutFinal : p.o_f32_recv ? kOutPaired : kOutPartial;
+  if (d == 64) return launch_fwd_d<64>(p, heads_per_tile, out, s);
+  if (d == 128) return launch_fwd_d<128>(p, heads_per_tile, out, s);
   return hipErrorInvalidValue;
 }
 

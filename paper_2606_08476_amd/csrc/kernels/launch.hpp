@@ -23,11 +23,11 @@ struct FwdParams {
   float* o_f32;
   float* lse;               // [hq, t_q]
   int32_t t_q;
-  // partial outputs of items with index < n_first (0: none), used when one
-  // launch runs both partial passes
-  int32_t n_first;
-  float* o_f32_first;
-  float* lse_first;
+  // both partials at once (non-null o_f32_recv): items carry a received and
+  // a local range; the received partial goes to o_f32_recv/lse_recv, the
+  // local one to o_f32/lse
+  float* o_f32_recv;
+  float* lse_recv;
 };
 
 struct BwdParams {
