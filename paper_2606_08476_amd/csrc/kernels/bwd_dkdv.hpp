@@ -59,6 +59,26 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   float* dVg = src ? p.dv_recv : p.dv_loc;
   const size_t kvs = size_t(p.hkv) * D, kvo = size_t(kvh) * D;
 
+  // first query row that sees this wave's first key: local rows from the
+  // key's own index on; received rows once their receive limit exceeds it
+  // (limits do not decrease along a segment: binary search). Read here,
+  // before the first asynchronous copy, so that the loads are scalar: after
+  // it the compiler treats memory as clobbered and would use vector loads,
+  // whose wait would also wait for the copies in flight.
+  const int kw = k0 + 32 * wave;
+  int qfirst = kw;
+  if (src) {
+    int lo = q0, hi = q1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (p.lim[mid] > kw)
+        hi = mid;
+      else
+        lo = mid + 1;
+    }
+    qfirst = lo;
+  }
+
   // key tile (rows past k1 repeat the last key; they are masked)
   TileLoader<D, BN>(p.hkv * D).load_at(lds_addr(smem) + OK, Kg + size_t(k0) * kvs + kvo, k1 - k0);
   const int kidx = k0 + 32 * wave + (lane & 31);  // this lane's key
@@ -195,7 +215,10 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
               const int g = e >> 2, j = e & 3, cq = 8 * g + j;
-              const int lim = j == 0 ? m4[g].x : j == 1 ? m4[g].y : j == 2 ? m4[g].z : m4[g].w;
+              // (local tiles never copy limits into LDS: what is there is
+              // stale and must not be compared)
+              const int lim = !src ? 0x7fffffff
+                              : j == 0 ? m4[g].x : j == 1 ? m4[g].y : j == 2 ? m4[g].z : m4[g].w;
               sacc[e] = ((cq >= lo) & (cq < hiq) & (kl < lim)) ? sacc[e] : 0.f;
             }
             pa[0] = pack8(sacc, 0);
@@ -221,18 +244,15 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   // wait for the copies. Each wave picks its own variant of the compute:
   // unmasked where every row of the tile sees all of the wave's 32 keys
   // (past the diagonal, a whole tile of rows, all keys in range); skipped
-  // where no row sees any of them (local keys after the tile's last row,
-  // received keys at or past every row's receive limit -- the limits do not
-  // decrease along a segment, so the last row's is the largest -- and keys
-  // past the range); masked otherwise.
+  // where no row sees any of them (the tile ends before qfirst, or the keys
+  // are past the range); masked otherwise.
   auto step = [&](int i_, auto bufc) {
     const int t0 = q0 + (i_ % ntile) * BM;
     if (i_ + 1 < n_it) fetch(i_ + 1, decltype(bufc)::value ^ 1);
     pr = opaque(pr);
     pt = opaque(pt);
-    const int kw = k0 + 32 * wave;
     const int tlast = min(t0 + BM, q1) - 1;
-    if (!(kw >= k1 || (src ? p.lim[tlast] <= kw : tlast < kw)))
+    if (!(kw >= k1 || tlast < qfirst))
       tile(t0, bufc, !(t0 >= qfull && t0 + BM <= q1 && kw + 32 <= k1));
     wait_async();
     __syncthreads();

@@ -215,7 +215,6 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
 }
 
-// Index of this thread's wave in the workgroup, as a wave-uniform value.
 // Calls f(std::integral_constant<int, I>()) for I = B .. E-1: a fully
 // unrolled loop whose index is a compile-time constant, whatever the size of
 // the body (a plain unroll pragma gives up past the unroller's size limit).
@@ -227,6 +226,7 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// Index of this thread's wave in the workgroup, as a wave-uniform value.
 __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
