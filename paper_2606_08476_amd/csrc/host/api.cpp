@@ -104,6 +104,7 @@ fck::BwdParams bwd_params(const View& v, const void* q, const void* k_loc, const
   p.items = m + v.off.bwd_launch;
   p.perm = m + v.off.perm_bwd_launch;
   p.lim = m + v.off.lim;
+  p.qfirst = m + v.off.bwd_qfirst;
   p.n_items = int32_t(v.bwd_launch.size() / 8);
   p.part_k = static_cast<float*>(ws);
   p.part_v = part ? reinterpret_cast<float*>(static_cast<char*>(ws) + part / 2) : nullptr;

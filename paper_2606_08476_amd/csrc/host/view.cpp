@@ -162,6 +162,24 @@ void View::build_bwd_launch() {
     bwd_reduce[bwd_reduce.size() - 4] = made;
   }
   perm_bwd_launch = lpt_order(cost);
+  // per launch item and wave (32 keys from k0 + 32w): the first query row
+  // that sees the wave's first key -- for local keys the key's own index,
+  // for received keys the first row whose receive limit exceeds it (limits
+  // do not decrease along a segment)
+  bwd_qfirst.clear();
+  for (size_t i = 0; i < bwd_launch.size() / 8; ++i) {
+    const int32_t* it = &bwd_launch[8 * i];
+    for (int32_t w = 0; w < bn_bwd / 32; ++w) {
+      const int32_t kw = it[0] + 32 * w;
+      int32_t qf = kw;
+      if (it[5]) {
+        const int32_t* b = lim.data() + it[2];
+        const int32_t* e = lim.data() + it[3];
+        qf = it[2] + int32_t(std::upper_bound(b, e, kw) - b);
+      }
+      bwd_qfirst.push_back(qf);
+    }
+  }
 }
 
 void View::build_meta() {
@@ -186,6 +204,7 @@ void View::build_meta() {
   off.bwd_launch = put(bwd_launch);
   off.perm_bwd_launch = put(perm_bwd_launch);
   off.bwd_reduce = put(bwd_reduce);
+  off.bwd_qfirst = put(bwd_qfirst);
   if (meta.empty()) meta.resize(64, 0);
 }
 

@@ -27,6 +27,8 @@ struct View {
   // (src, k0, k1, first slot, slot count, 0, 0, 0)
   std::vector<int32_t> bwd_launch, perm_bwd_launch, bwd_reduce;
   int32_t n_bwd_slots = 0;
+  // per launch item, per 32-key wave: first query row that sees its first key
+  std::vector<int32_t> bwd_qfirst;
 
   // device blob: every table above that a kernel reads, int32, sections
   // aligned to 256 bytes; `off` holds section offsets in int32 elements
@@ -35,7 +37,7 @@ struct View {
     int64_t fwd_local, fwd_recv, fwd_fused, bwd;
     int64_t perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
     int64_t q_gpos, recv_gpos, lim;
-    int64_t bwd_launch, perm_bwd_launch, bwd_reduce;
+    int64_t bwd_launch, perm_bwd_launch, bwd_reduce, bwd_qfirst;
   } off{};
   const int32_t* dev_meta = nullptr;        // set by fc_view_bind
 

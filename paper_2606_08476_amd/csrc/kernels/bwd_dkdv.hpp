@@ -51,7 +51,8 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5;
   const int kvh = b % p.hkv;
-  const int32_t* it = p.items + 8 * p.perm[b / p.hkv];  // launch list
+  const int item = p.perm[b / p.hkv];
+  const int32_t* it = p.items + 8 * item;  // launch list
   const int k0 = it[0], k1 = it[1], q0 = it[2], q1 = it[3], qfull = it[4], src = it[5];
   const u16* Kg = src ? p.k_recv : p.k_loc;
   const u16* Vg = src ? p.v_recv : p.v_loc;
@@ -59,25 +60,11 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   float* dVg = src ? p.dv_recv : p.dv_loc;
   const size_t kvs = size_t(p.hkv) * D, kvo = size_t(kvh) * D;
 
-  // first query row that sees this wave's first key: local rows from the
-  // key's own index on; received rows once their receive limit exceeds it
-  // (limits do not decrease along a segment: binary search). Read here,
-  // before the first asynchronous copy, so that the loads are scalar: after
-  // it the compiler treats memory as clobbered and would use vector loads,
-  // whose wait would also wait for the copies in flight.
+  // first query row that sees this wave's first key (host table: local rows
+  // from the key's own index on, received rows once their receive limit
+  // exceeds it)
   const int kw = k0 + 32 * wave;
-  int qfirst = kw;
-  if (src) {
-    int lo = q0, hi = q1;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (p.lim[mid] > kw)
-        hi = mid;
-      else
-        lo = mid + 1;
-    }
-    qfirst = lo;
-  }
+  const int qfirst = p.qfirst[4 * item + wave];
 
   // key tile (rows past k1 repeat the last key; they are masked)
   TileLoader<D, BN>(p.hkv * D).load_at(lds_addr(smem) + OK, Kg + size_t(k0) * kvs + kvo, k1 - k0);

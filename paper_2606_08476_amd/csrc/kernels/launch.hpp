@@ -42,6 +42,7 @@ struct BwdParams {
   const int32_t* items;     // 8 int32 per item: k0 k1 q0 q1 qfull src seg slot
   const int32_t* perm;
   const int32_t* lim;       // [t_q] receive index end per query
+  const int32_t* qfirst;    // per item, per 32-key wave: first query row that sees it
   float* part_k;            // [slots, hkv, 128, d] partial dK/dV of split key tiles
   float* part_v;
   int32_t n_items;
