@@ -5,7 +5,8 @@
 A step is the whole path once over one synthetic packed sequence: the shard
 plan and rank view (host, C++), the table upload, the KV gather that stands
 in for the sharding-aware receive, the local and received forward partial
-passes (one launch), their log-sum-exp merge, the backward preprocess, and
+passes and their log-sum-exp merge (one launch: each workgroup merges its
+query tile's two partials in its epilogue), the backward preprocess, and
 the key-major dK/dV and query-major dQ passes.
 Inputs are resident in HBM before timing starts. The metric counts useful
 FLOPs: 14 * d * Hq * pairs, pairs being the visible (query, key) pairs per
@@ -269,20 +270,16 @@ def study_granularity(args):
                 e = lambda *sh, dt=f32: torch.empty(*sh, dtype=dt, device=dev)
                 kl, vl = e(tq, hkv, d, dt=bf), e(tq, hkv, d, dt=bf)
                 kr, vr = e(tr, hkv, d, dt=bf), e(tr, hkv, d, dt=bf)
-                oa, ob, la, lb = e(tq, hq, d), e(tq, hq, d), e(hq, tq), e(hq, tq)
                 o, lse, delta = e(tq, hq, d, dt=bf), e(hq, tq), e(hq, tq)
                 dq, dkl, dvl = e(tq, hq, d), e(tq, hkv, d), e(tq, hkv, d)
                 dkr, dvr = e(tr, hkv, d), e(tr, hkv, d)
                 ws = torch.empty(max(v.workspace_size()[2], 1), dtype=torch.uint8, device=dev)
-                no_ws = torch.empty(1, dtype=torch.uint8, device=dev)
+                fws = torch.empty(max(v.workspace_size(F.FC_TWO_PASS)[0], 1), dtype=torch.uint8,
+                                  device=dev)
 
                 def run():
                     F.fc_kv_gather(v, k_pk, v_pk, kl, vl, kr, vr)
-                    if tr:
-                        F.fc_attn_fwd_partials(v, q, kl, vl, kr, vr, 0.0, oa, la, ob, lb)
-                        F.fc_lse_merge(oa, la, ob, lb, o, None, lse)
-                    else:
-                        F.fc_attn_fwd(v, q, kl, vl, kr, vr, 0.0, F.FC_TWO_PASS, o, None, lse, no_ws)
+                    F.fc_attn_fwd(v, q, kl, vl, kr, vr, 0.0, F.FC_TWO_PASS, o, None, lse, fws)
                     F.fc_bwd_preprocess(v, o, do, delta)
                     F.fc_attn_bwd_pass(v, q, kl, vl, kr, vr, lse, delta, do, 0.0, dq, dkl, dvl, dkr, dvr, ws)
 
@@ -363,10 +360,6 @@ def main():
     v_loc = torch.empty_like(k_loc)
     k_recv = torch.empty(tr, hkv, d, dtype=bf, device=dev)
     v_recv = torch.empty_like(k_recv)
-    o_a = torch.empty(tq, hq, d, dtype=f32, device=dev)
-    o_b = torch.empty_like(o_a)
-    l_a = torch.empty(hq, tq, dtype=f32, device=dev)
-    l_b = torch.empty_like(l_a)
     o = torch.empty(tq, hq, d, dtype=bf, device=dev)
     lse = torch.empty(hq, tq, dtype=f32, device=dev)
     delta = torch.empty(hq, tq, dtype=f32, device=dev)
@@ -376,9 +369,9 @@ def main():
     dk_recv = torch.empty(tr, hkv, d, dtype=f32, device=dev)
     dv_recv = torch.empty_like(dk_recv)
     meta = torch.empty(int(info["meta_bytes"]) + 256, dtype=torch.uint8, device=dev)
-    no_ws = torch.empty(0, dtype=torch.uint8, device=dev)
+    fwd_ws = torch.empty(max(view.workspace_size(F.FC_TWO_PASS)[0], 1), dtype=torch.uint8, device=dev)
     dkdv_ws = torch.empty(view.workspace_size()[2], dtype=torch.uint8, device=dev)
-    names = ["kv_gather", "attn_fwd_partials", "lse_merge", "bwd_preprocess", "attn_bwd"]
+    names = ["kv_gather", "attn_fwd", "bwd_preprocess", "attn_bwd"]
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
     acc = np.zeros(len(names))
     kept = []
@@ -390,22 +383,17 @@ def main():
         ev[0].record()
         F.fc_kv_gather(v, k_pk, v_pk, k_loc, v_loc, k_recv, v_recv)
         ev[1].record()
-        if tr:
-            # both partial passes (local keys, received keys) in one launch
-            F.fc_attn_fwd_partials(v, q, k_loc, v_loc, k_recv, v_recv, 0.0, o_a, l_a, o_b, l_b)
-            ev[2].record()
-            F.fc_lse_merge(o_a, l_a, o_b, l_b, o, None, lse)
-        else:
-            # no received KV: the local pass alone writes the final O and LSE
-            F.fc_attn_fwd(v, q, k_loc, v_loc, k_recv, v_recv, 0.0, F.FC_TWO_PASS, o, None, lse, no_ws)
-            ev[2].record()
-        ev[3].record()
+        # both partial passes (received keys, then local keys) and their
+        # log-sum-exp merge in one launch; with no received KV the local pass
+        # alone writes the final O and LSE
+        F.fc_attn_fwd(v, q, k_loc, v_loc, k_recv, v_recv, 0.0, F.FC_TWO_PASS, o, None, lse, fwd_ws)
+        ev[2].record()
         F.fc_bwd_preprocess(v, o, do, delta)
-        ev[4].record()
+        ev[3].record()
         # dK/dV (key-major) and dQ (query-major) workgroups in one launch
         F.fc_attn_bwd_pass(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq, dk_loc,
                            dv_loc, dk_recv, dv_recv, dkdv_ws)
-        ev[5].record()
+        ev[4].record()
 
     for _ in range(args.warmup):
         step(False)
@@ -435,8 +423,8 @@ def main():
     kv_rows = tq + tr
     work = {
         "kv_gather": ("hbm", 2 * 2 * kv_rows * hkv * d * 2),
-        "attn_fwd_partials": ("mfma", 4.0 * d * hq * pairs),
-        "lse_merge": ("hbm", tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4) if tr else 0),
+        # both partial passes (4d per pair) with the merge in their epilogue
+        "attn_fwd": ("mfma", 4.0 * d * hq * pairs),
         "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4)),
         # backward, algorithmic: S recomputed once, dP, dV, dK, dQ (10d per
         # pair, the FlashAttention count); the kernels execute 14d (the dQ
@@ -449,7 +437,7 @@ def main():
         kind, amount = work[n]
         t = acc[i] * 1e-3
         if amount == 0 or acc[i] <= 0:
-            kernels[n] = {"ms": round(acc[i], 4), "skipped": "no received KV (no merge)"}
+            kernels[n] = {"ms": round(acc[i], 4)}
             continue
         if kind == "mfma":
             a = amount / t / 1e12
@@ -479,7 +467,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.context}-token packed context, CP degree {w.cp}, "
                                f"{w.plan} plan, rank {rank}; {hq} query / {hkv} KV heads, d {d}; "
-                               "two-pass forward (local and received partials in one launch) + LSE merge, "
+                               "two-pass forward (received and local partials and their LSE merge in one launch), "
                                "key-major dK/dV and query-major dQ backward",
                    "t_q": tq, "t_recv": tr, "pairs_per_head": pairs,
                    "useful_tflop_per_step": round(useful / 1e12, 4),

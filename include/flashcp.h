@@ -203,7 +203,10 @@ int fc_kv_gather(fc_view view, const void* k_packed, const void* v_packed, int64
 
 /* Forward. Writes o (bf16 [T_q,Hq,d]), optionally o_f32 (fp32, same shape;
  * NULL to skip) and lse (fp32 [Hq,T_q]). FC_TWO_PASS runs the local and the
- * received pass into the workspace and merges them; FC_FUSED computes
+ * received pass (Sec. 3.2) and their log-sum-exp merge in one launch: each
+ * query tile's received partial O goes to the workspace and is merged with
+ * its local partial in the kernel; o and lse are exactly what
+ * fc_attn_fwd_partials followed by fc_lse_merge write. FC_FUSED computes
  * both sources in one online softmax. ws: device, >= fc_workspace_size. */
 int fc_attn_fwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                 const void* k_recv, const void* v_recv, float scale, int32_t mode,
@@ -216,8 +219,8 @@ int fc_attn_fwd_partial(fc_view view, int32_t src, const void* q, const void* k_
                         const void* v_src, float scale, float* o_part, float* lse_part,
                         void* stream);
 
-/* Both partial passes in one launch (the two-pass forward's first step;
- * fc_attn_fwd with FC_TWO_PASS uses it): local keys into o_loc/lse_loc,
+/* Both partial passes in one launch (the two-pass forward's first step,
+ * for a caller that merges later): local keys into o_loc/lse_loc,
  * received keys into o_recv/lse_recv, with the shapes and the empty-row
  * rule of fc_attn_fwd_partial; results are identical to the two separate
  * calls. k_recv/v_recv may be NULL when the view receives no keys (the

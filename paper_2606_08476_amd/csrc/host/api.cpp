@@ -34,12 +34,13 @@ float resolve_scale(float scale, int d) { return scale > 0.f ? scale : 1.f / std
 struct FwdWs {
   size_t o_bytes, l_bytes, total;
 };
+// FC_TWO_PASS with received keys: the received partial's fp32 O (the
+// kernel merges it with the local partial in its epilogue)
 FwdWs fwd_ws(const View& v, int32_t mode) {
   FwdWs w{};
   if (mode == FC_TWO_PASS && v.t_recv() > 0) {
     w.o_bytes = align_up(size_t(v.t_q()) * v.hq * v.d * sizeof(float));
-    w.l_bytes = align_up(size_t(v.t_q()) * v.hq * sizeof(float));
-    w.total = 2 * (w.o_bytes + w.l_bytes);
+    w.total = w.o_bytes;
   }
   return w;
 }
@@ -269,16 +270,17 @@ int fc_attn_fwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
     p.lse = lse;
     return hip_status(fck::launch_fwd(p, v->d, v->heads_per_tile, true, s), "attn_fwd launch");
   }
-  char* base = static_cast<char*>(ws);
-  float* oa = reinterpret_cast<float*>(base);
-  float* ob = reinterpret_cast<float*>(base + w.o_bytes);
-  float* la = reinterpret_cast<float*>(base + 2 * w.o_bytes);
-  float* lb = reinterpret_cast<float*>(base + 2 * w.o_bytes + w.l_bytes);
-  if (int rc = launch_partials(*v, q, k_loc, v_loc, k_recv, v_recv, scale, oa, la, ob, lb, s))
-    return rc;
-  return hip_status(fck::launch_lse_merge(oa, la, ob, lb, v->t_q(), v->hq, v->d,
-                                          static_cast<uint16_t*>(o), o_f32, lse, s),
-                    "lse_merge launch");
+  // both partial passes and their log-sum-exp merge in one launch: each
+  // workgroup runs its query tile's received range (partial O to the
+  // workspace), then its local range, and merges the two in its epilogue
+  fck::FwdParams p = fwd_params(*v, m + v->off.fwd_fused, m + v->off.perm_fwd_fused,
+                                int64_t(v->fwd_fused.size() / 8), q, k_loc, v_loc, k_recv,
+                                v_recv, scale);
+  p.o_f32_recv = static_cast<float*>(ws);
+  p.o_bf16 = static_cast<uint16_t*>(o);
+  p.o_f32 = o_f32;
+  p.lse = lse;
+  return hip_status(fck::launch_fwd(p, v->d, v->heads_per_tile, true, s), "attn_fwd launch");
 }
 
 int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const float* lse_b,

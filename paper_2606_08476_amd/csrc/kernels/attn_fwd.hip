@@ -24,7 +24,11 @@
 // fp32 partial O/LSE for the log-sum-exp merge; or, for items that carry a
 // received and a local range, both partials: the received range is run
 // first and its partial written when the local range starts, so the query
-// tile is loaded once and the tile pipeline runs on across the switch.
+// tile is loaded once and the tile pipeline runs on across the switch; or
+// (merged) the same two passes followed by their log-sum-exp merge in the
+// epilogue: the received partial's O is written to a workspace at the
+// switch and read back at the end, its LSE kept in a register, and the
+// final O and LSE are written as the merge kernel would write them.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -32,11 +36,12 @@
 
 namespace fck {
 
-enum { kOutPartial = 0, kOutFinal = 1, kOutPaired = 2 };
+enum { kOutPartial = 0, kOutFinal = 1, kOutPaired = 2, kOutMerged = 3 };
 
 template <int D, int HPW, int OUT>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
-  constexpr bool FINAL = OUT == kOutFinal, PAIRED = OUT == kOutPaired;
+  constexpr bool FINAL = OUT == kOutFinal, MERGED = OUT == kOutMerged;
+  constexpr bool PAIRED = OUT == kOutPaired || MERGED;
   constexpr int BN = 64;        // keys per tile
   constexpr int WPH = 4 / HPW;  // waves per query head
   constexpr int KS = D / 16;    // MFMA k-steps over the head dim
@@ -135,13 +140,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
           if (!FINAL || o_out) *reinterpret_cast<f32x4*>(o_out + ob + dcol) = v;
         }
       }
-      if (half == 0) lse_out[(size_t)h * p.t_q + qrow] = lse;
+      if (half == 0 && lse_out) lse_out[(size_t)h * p.t_q + qrow] = lse;
     }
   };
   // paired items: the received partial is complete when the local range
   // starts; write it and start the local one from empty
+  float lse_recv = -INFINITY;  // merged: the received partial's LSE
   auto switch_source = [&]() {
-    write_out(p.o_f32_recv, p.lse_recv);
+    if (MERGED) {
+      const float tot = lsum + __shfl_xor(lsum, 32);
+      lse_recv = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
+    }
+    write_out(p.o_f32_recv, MERGED ? nullptr : p.lse_recv);
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = zero16();
     m = -INFINITY;
@@ -235,7 +245,37 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   }
 
   if (PAIRED && n_r == n_t) switch_source();  // no local tile (never empty in practice)
-  write_out(p.o_f32, p.lse);
+  if constexpr (MERGED) {
+    // local partial (registers) merged with the received one (workspace,
+    // written by this lane at the switch; the waits since have completed it)
+    wait_async();
+    const float tot = lsum + __shfl_xor(lsum, 32);
+    const float inv = tot > 0.f ? 1.f / tot : 0.f;
+    const float lse_loc = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
+    const Merge2 w = merge2(lse_loc, lse_recv);
+    if (qvalid) {
+      const size_t ob = ((size_t)qrow * p.hq + h) * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int dcol = 32 * db + 8 * g + 4 * half;
+          const f32x4 y = *reinterpret_cast<const f32x4*>(p.o_f32_recv + ob + dcol);
+          f32x4 v;
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) v[jj] = merge2_value(w, oacc[db][4 * g + jj] * inv, y[jj]);
+          uint2 packed;
+          packed.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
+          packed.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
+          *reinterpret_cast<uint2*>(p.o_bf16 + ob + dcol) = packed;
+          if (p.o_f32) *reinterpret_cast<f32x4*>(p.o_f32 + ob + dcol) = v;
+        }
+      }
+      if (half == 0) p.lse[(size_t)h * p.t_q + qrow] = w.lse;
+    }
+  } else {
+    write_out(p.o_f32, p.lse);
+  }
 }
 
 template <int D, int HPW>
@@ -245,6 +285,8 @@ static hipError_t launch_fwd_t(const FwdParams& p, int out, hipStream_t s) {
     hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, kOutFinal>), grid, block, 0, s, p);
   else if (out == kOutPaired)
     hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, kOutPaired>), grid, block, 0, s, p);
+  else if (out == kOutMerged)
+    hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, kOutMerged>), grid, block, 0, s, p);
   else
     hipLaunchKernelGGL((attn_fwd_kernel<D, HPW, kOutPartial>), grid, block, 0, s, p);
   return hipGetLastError();
@@ -263,7 +305,8 @@ static hipError_t launch_fwd_d(const FwdParams& p, int hpw, int out, hipStream_t
 hipError_t launch_fwd(const FwdParams& p, int d, int heads_per_tile, bool final_out,
                       hipStream_t s) {
   if (p.n_items == 0) return hipSuccess;
-  const int out = final_out ? kOutFinal : p.o_f32_recv ? kOutPaired : kOutPartial;
+  const int out = p.o_f32_recv ? (final_out ? kOutMerged : kOutPaired)
+                  : final_out ? kOutFinal : kOutPartial;
   if (d == 64) return launch_fwd_d<64>(p, heads_per_tile, out, s);
   if (d == 128) return launch_fwd_d<128>(p, heads_per_tile, out, s);
   return hipErrorInvalidValue;

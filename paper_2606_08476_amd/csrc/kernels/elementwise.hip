@@ -44,23 +44,18 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const float* __restrict_
   if (row >= int64_t(t) * h) return;
   const int32_t tok = int32_t(row / h), head = int32_t(row % h);
   const int64_t li = int64_t(head) * t + tok;
-  const float a = la[li], bb = lb[li];
-  const float mx = fmaxf(a, bb);
-  const float m = mx == -INFINITY ? 0.f : mx;
-  const float wa = __expf(a - m), wb = __expf(bb - m);
-  const float tot = wa + wb;
-  const float ca = wa / tot, cb = wb / tot;
+  const Merge2 w = merge2(la[li], lb[li]);
   const f32x4 x = reinterpret_cast<const f32x4*>(oa + row * D)[c];
   const f32x4 y = reinterpret_cast<const f32x4*>(ob + row * D)[c];
   f32x4 r;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) r[j] = ca * x[j] + cb * y[j];
+  for (int j = 0; j < 4; ++j) r[j] = merge2_value(w, x[j], y[j]);
   uint2 pk;
   pk.x = uint32_t(f2bf(r[0])) | (uint32_t(f2bf(r[1])) << 16);
   pk.y = uint32_t(f2bf(r[2])) | (uint32_t(f2bf(r[3])) << 16);
   reinterpret_cast<uint2*>(o + row * D)[c] = pk;
   if (of) reinterpret_cast<f32x4*>(of + row * D)[c] = r;
-  if (c == 0) lse_out[li] = m + __logf(tot);
+  if (c == 0) lse_out[li] = w.lse;
 }
 
 // delta[head, tok] = sum_d dO * O over one (token, head) row.

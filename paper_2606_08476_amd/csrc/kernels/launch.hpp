@@ -25,7 +25,9 @@ struct FwdParams {
   int32_t t_q;
   // both partials at once (non-null o_f32_recv): items carry a received and
   // a local range; the received partial goes to o_f32_recv/lse_recv, the
-  // local one to o_f32/lse
+  // local one to o_f32/lse; with final output, the two are merged in the
+  // kernel (o_f32_recv is then a workspace, lse_recv unused) and the final
+  // O/LSE written as for the one-pass final output
   float* o_f32_recv;
   float* lse_recv;
 };

@@ -193,6 +193,20 @@ def test_partial_passes_and_merge(key, dev):
     torch.cuda.synchronize()
     for (op, lp), oc, lc in zip(sep, o2, l2):
         assert torch.equal(op, oc) and torch.equal(lp, lc)
+    # the two-pass forward (both passes and their merge in one launch) writes
+    # exactly what the partial passes followed by the merge kernel write
+    if i["t_recv"]:
+        e3 = lambda dt=torch.float32: (torch.empty(tq, hq, d, dtype=torch.bfloat16, device=dev),
+                                        torch.empty(tq, hq, d, dtype=torch.float32, device=dev),
+                                        torch.empty(hq, tq, dtype=torch.float32, device=dev))
+        ob1, of1, lo1 = e3()
+        F.fc_lse_merge(o2[0], l2[0], o2[1], l2[1], ob1, of1, lo1)
+        ob2, of2, lo2 = e3()
+        ws = torch.empty(max(r.v.workspace_size(F.FC_TWO_PASS)[0], 1), dtype=torch.uint8, device=dev)
+        F.fc_attn_fwd(r.v, r.q, r.k_loc, r.v_loc, r.k_recv, r.v_recv, 0.0, F.FC_TWO_PASS, ob2, of2,
+                      lo2, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(ob1, ob2) and torch.equal(of1, of2) and torch.equal(lo1, lo2)
     # the merge kernel on the oracle's partials against the oracle's merge
     (Oa, La), (Ob, Lb) = outs
     Om, Lm = A.lse_merge(Oa, La, Ob, Lb)
