@@ -412,6 +412,28 @@ def main():
         for i in range(len(names)):
             acc[i] += e[i].elapsed_time(e[i + 1])
     acc /= args.steps
+    # the merge kernel alone (outside the timed steps): the step merges in the
+    # forward's epilogue, this is fc_lse_merge for partials made apart
+    merge_side = None
+    if tr:
+        o_a, o_b = (torch.empty(tq, hq, d, dtype=f32, device=dev) for _ in range(2))
+        l_a, l_b = (torch.empty(hq, tq, dtype=f32, device=dev) for _ in range(2))
+        F.fc_attn_fwd_partials(kept[-1], q, k_loc, v_loc, k_recv, v_recv, 0.0, o_a, l_a, o_b, l_b)
+        me = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for _ in range(3):
+            F.fc_lse_merge(o_a, l_a, o_b, l_b, o, None, lse)
+        me[0].record()
+        for _ in range(20):
+            F.fc_lse_merge(o_a, l_a, o_b, l_b, o, None, lse)
+        me[1].record()
+        torch.cuda.synchronize()
+        mms = me[0].elapsed_time(me[1]) / 20
+        gbs = tq * hq * (2 * 4 * d + 2 * 4 + 2 * d + 4) / (mms * 1e-3) / 1e9
+        merge_side = {"ms": round(mms, 4), "gbs": round(gbs, 1),
+                      "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+                      "note": "fc_lse_merge alone, not in the step (the step merges in the forward)"}
+        del o_a, o_b, l_a, l_b
+
     for v in kept:
         v.close()
     kept.clear()
@@ -475,6 +497,7 @@ def main():
                    "strict_tflops_12d": round(12.0 * d * hq * pairs / (ms * 1e-3) / 1e12, 2)},
         "roofline": roof,
         "kernels": kernels,
+        "lse_merge_alone": merge_side,
     }
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(cu, tab, x, w, args.cpu_seconds)
