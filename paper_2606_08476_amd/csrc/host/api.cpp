@@ -50,7 +50,7 @@ size_t part_ws(const View& v) {
 }
 size_t bwd_ws(const View& v) { return delta_ws(v) + part_ws(v); }
 
-fck::FwdParams fwd_params(const View& v, const int32_t* items, const int32_t* perm, int64_t n,
+fck::FwdParams fwd_params(const View& v, const int32_t* items, int64_t n,
                           const void* q, const void* k_loc, const void* v_loc, const void* k_recv,
                           const void* v_recv, float scale) {
   fck::FwdParams p{};
@@ -60,7 +60,6 @@ fck::FwdParams fwd_params(const View& v, const int32_t* items, const int32_t* pe
   p.k_recv = static_cast<const uint16_t*>(k_recv);
   p.v_recv = static_cast<const uint16_t*>(v_recv);
   p.items = items;
-  p.perm = perm;
   p.n_items = int32_t(n);
   p.hq = v.hq;
   p.hkv = v.hkv;
@@ -78,7 +77,7 @@ int launch_partials(const View& v, const void* q, const void* k_loc, const void*
                     const void* k_recv, const void* v_recv, float scale, float* o_loc,
                     float* lse_loc, float* o_recv, float* lse_recv, hipStream_t s) {
   const int32_t* m = v.dev_meta;
-  fck::FwdParams p = fwd_params(v, m + v.off.fwd_fused, m + v.off.perm_fwd_fused,
+  fck::FwdParams p = fwd_params(v, m + v.off.fwd_fused,
                                 int64_t(v.fwd_fused.size() / 8), q, k_loc, v_loc, k_recv, v_recv,
                                 scale);
   p.o_f32 = o_loc;
@@ -103,7 +102,6 @@ fck::BwdParams bwd_params(const View& v, const void* q, const void* k_loc, const
   p.k_recv = static_cast<const uint16_t*>(k_recv);
   p.v_recv = static_cast<const uint16_t*>(v_recv);
   p.items = m + v.off.bwd_launch;
-  p.perm = m + v.off.perm_bwd_launch;
   p.lim = m + v.off.lim;
   p.qfirst = m + v.off.bwd_qfirst;
   p.n_items = int32_t(v.bwd_launch.size() / 8);
@@ -135,7 +133,6 @@ fck::DqParams dq_params(const View& v, const void* q, const void* k_loc, const v
   d.k_recv = static_cast<const uint16_t*>(k_recv);
   d.v_recv = static_cast<const uint16_t*>(v_recv);
   d.items = m + v.off.fwd_fused;
-  d.perm = m + v.off.perm_fwd_fused;
   d.n_items = int32_t(v.fwd_fused.size() / 8);
   d.hq = v.hq;
   d.hkv = v.hkv;
@@ -213,10 +210,10 @@ int fc_attn_fwd_partial(fc_view view, int32_t src, const void* q, const void* k_
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
   const int32_t* m = v->dev_meta;
   fck::FwdParams p =
-      src == 0 ? fwd_params(*v, m + v->off.fwd_local, m + v->off.perm_fwd_local,
+      src == 0 ? fwd_params(*v, m + v->off.fwd_local,
                             int64_t(v->fwd_local.size() / 8), q, k_src, v_src, nullptr, nullptr,
                             scale)
-               : fwd_params(*v, m + v->off.fwd_recv, m + v->off.perm_fwd_recv,
+               : fwd_params(*v, m + v->off.fwd_recv,
                             int64_t(v->fwd_recv.size() / 8), q, nullptr, nullptr, k_src, v_src,
                             scale);
   p.o_f32 = o_part;
@@ -260,9 +257,9 @@ int fc_attn_fwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
     // one pass: both sources (fused items), or the local source alone
     const bool fused = mode == FC_FUSED && v->t_recv() > 0;
     fck::FwdParams p =
-        fused ? fwd_params(*v, m + v->off.fwd_fused, m + v->off.perm_fwd_fused,
+        fused ? fwd_params(*v, m + v->off.fwd_fused,
                            int64_t(v->fwd_fused.size() / 8), q, k_loc, v_loc, k_recv, v_recv, scale)
-              : fwd_params(*v, m + v->off.fwd_local, m + v->off.perm_fwd_local,
+              : fwd_params(*v, m + v->off.fwd_local,
                            int64_t(v->fwd_local.size() / 8), q, k_loc, v_loc, nullptr, nullptr,
                            scale);
     p.o_bf16 = static_cast<uint16_t*>(o);
@@ -273,7 +270,7 @@ int fc_attn_fwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
   // both partial passes and their log-sum-exp merge in one launch: each
   // workgroup runs its query tile's received range (partial O to the
   // workspace), then its local range, and merges the two in its epilogue
-  fck::FwdParams p = fwd_params(*v, m + v->off.fwd_fused, m + v->off.perm_fwd_fused,
+  fck::FwdParams p = fwd_params(*v, m + v->off.fwd_fused,
                                 int64_t(v->fwd_fused.size() / 8), q, k_loc, v_loc, k_recv,
                                 v_recv, scale);
   p.o_f32_recv = static_cast<float*>(ws);

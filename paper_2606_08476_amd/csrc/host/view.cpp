@@ -161,7 +161,15 @@ void View::build_bwd_launch() {
     }
     bwd_reduce[bwd_reduce.size() - 4] = made;
   }
-  perm_bwd_launch = lpt_order(cost);
+  // the launch list itself goes in largest-first order: workgroup b takes
+  // item b / hkv, with no order table to read first
+  {
+    const std::vector<int32_t> order = lpt_order(cost);
+    std::vector<int32_t> sorted;
+    sorted.reserve(bwd_launch.size());
+    for (int32_t i : order) sorted.insert(sorted.end(), &bwd_launch[8 * i], &bwd_launch[8 * i + 8]);
+    bwd_launch.swap(sorted);
+  }
   // per launch item and wave (32 keys from k0 + 32w): the first query row
   // that sees the wave's first key -- for local keys the key's own index,
   // for received keys the first row whose receive limit exceeds it (limits
@@ -190,19 +198,21 @@ void View::build_meta() {
     meta.resize((meta.size() + 63) / 64 * 64, 0);  // 256-byte aligned sections
     return off;
   };
-  off.fwd_local = put(fwd_local);
-  off.fwd_recv = put(fwd_recv);
-  off.fwd_fused = put(fwd_fused);
-  off.bwd = put(bwd);
-  off.perm_fwd_local = put(perm_fwd_local);
-  off.perm_fwd_recv = put(perm_fwd_recv);
-  off.perm_fwd_fused = put(perm_fwd_fused);
-  off.perm_bwd = put(perm_bwd);
+  // forward item lists in their launch (largest-first) order: workgroup b
+  // reads its item directly, with no order table to read first
+  auto in_order = [](const std::vector<int32_t>& items, const std::vector<int32_t>& order) {
+    std::vector<int32_t> r;
+    r.reserve(items.size());
+    for (int32_t i : order) r.insert(r.end(), &items[8 * i], &items[8 * i + 8]);
+    return r;
+  };
+  off.fwd_local = put(in_order(fwd_local, perm_fwd_local));
+  off.fwd_recv = put(in_order(fwd_recv, perm_fwd_recv));
+  off.fwd_fused = put(in_order(fwd_fused, perm_fwd_fused));
   off.q_gpos = put(q_gpos);
   off.recv_gpos = put(recv_gpos);
   off.lim = put(lim);
   off.bwd_launch = put(bwd_launch);
-  off.perm_bwd_launch = put(perm_bwd_launch);
   off.bwd_reduce = put(bwd_reduce);
   off.bwd_qfirst = put(bwd_qfirst);
   if (meta.empty()) meta.resize(64, 0);

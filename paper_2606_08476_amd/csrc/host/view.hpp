@@ -18,26 +18,27 @@ struct View {
   std::vector<int32_t> lim;                 // receive index end seen by each query
   int64_t pairs_loc = 0, pairs_recv = 0;
 
-  // work lists, 8 int32 per item (layout documented in flashcp.h)
+  // work lists, 8 int32 per item (layout documented in flashcp.h), in map
+  // order, and their largest-first launch orders
   std::vector<int32_t> fwd_local, fwd_recv, fwd_fused, bwd;
   std::vector<int32_t> perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
-  // backward launch list: the key-major items with long query ranges split
-  // into parts that write partial dK/dV (last field: partial slot, -1 for a
-  // direct write), and one reduce entry per split key tile
+  // backward launch list, largest first: the key-major items with long query
+  // ranges split into parts that write partial dK/dV (last field: partial
+  // slot, -1 for a direct write), and one reduce entry per split key tile
   // (src, k0, k1, first slot, slot count, 0, 0, 0)
-  std::vector<int32_t> bwd_launch, perm_bwd_launch, bwd_reduce;
+  std::vector<int32_t> bwd_launch, bwd_reduce;
   int32_t n_bwd_slots = 0;
   // per launch item, per 32-key wave: first query row that sees its first key
   std::vector<int32_t> bwd_qfirst;
 
-  // device blob: every table above that a kernel reads, int32, sections
-  // aligned to 256 bytes; `off` holds section offsets in int32 elements
+  // device blob: every table above that a kernel reads (the forward lists in
+  // launch order), int32, sections aligned to 256 bytes; `off` holds section
+  // offsets in int32 elements
   std::vector<int32_t> meta;
   struct {
-    int64_t fwd_local, fwd_recv, fwd_fused, bwd;
-    int64_t perm_fwd_local, perm_fwd_recv, perm_fwd_fused, perm_bwd;
+    int64_t fwd_local, fwd_recv, fwd_fused;
     int64_t q_gpos, recv_gpos, lim;
-    int64_t bwd_launch, perm_bwd_launch, bwd_reduce, bwd_qfirst;
+    int64_t bwd_launch, bwd_reduce, bwd_qfirst;
   } off{};
   const int32_t* dev_meta = nullptr;        // set by fc_view_bind
 

@@ -6,9 +6,10 @@
 // (intra-document causal, Sec. 2.1) -- for `heads_per_tile` query heads of
 // one KV head. Each wave owns 32 query rows of one head. Key tiles of 64
 // keys are double-buffered in LDS and shared by the waves (and so by the
-// heads of the group); the next tile is copied from HBM straight into LDS
+// heads of the group); later tiles are copied from HBM straight into LDS
 // (asynchronous loads, no staging registers) while the current one is
-// computed:
+// computed, and the loop is software-pipelined across tiles (the scores of
+// the next tile are computed beside the softmax of the current one):
 //   S^T = K Q^T        MFMA 32x32x16, Q held in registers (B operand), so a
 //                      query is a lane and its row statistics are per lane;
 //   online softmax     base 2, scale folded into one FMA per score; a row's
@@ -48,8 +49,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   constexpr int DB = D / 32;    // 32-wide output blocks of the head dim
   constexpr float kLazy = 8.0f; // log2 headroom before rescaling
   constexpr uint32_t TILE = BN * D * 2;  // bytes of one K or V tile
-  // LDS: K0 | V0 | K1 | V1 (double buffer). The loop is unrolled by two, so
-  // every read names its buffer with a compile-time offset.
+  // LDS: K0 | K1 | V0 | V1; key tile j uses K buffer j % 2 and V buffer
+  // j % 2. K runs one tile ahead of V: iteration j reads K of tile j+1 and V
+  // of tile j while the copies of K of tile j+2 and V of tile j+1 fill the
+  // other two buffers. The loop is unrolled by two, so every read names its
+  // buffer with a compile-time offset.
   __shared__ __attribute__((aligned(16))) char smem[4 * TILE];
 
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -58,8 +62,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int kvh = b % p.hkv;
   const int rest = b / p.hkv;
   const int hc = rest % p.head_chunks;
-  const int item = p.perm[rest / p.head_chunks];
-  const int32_t* it = p.items + 8 * item;
+  const int32_t* it = p.items + 8 * (rest / p.head_chunks);
   const int q0 = it[0], q1 = it[1], r0 = it[2], r1 = it[3], l0 = it[4], l1 = it[5];
   const int ldiag = it[6];
 
@@ -72,20 +75,24 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int n_r = (r1 - r0 + BN - 1) / BN;
   const int n_t = n_r + (l1 - l0 + BN - 1) / BN;
 
-  // async copy of key tile j into the buffer at byte offset `kofs` (K, then
-  // V at +TILE); rows past the range repeat the last row (finite data; those
-  // keys are masked)
+  // async copy of the K (or V) rows of key tile j into the buffer at byte
+  // offset `ofs`; rows past the range repeat the last row (finite data;
+  // those keys are masked)
   const TileLoader<D, BN> ld(p.hkv * D);
-  auto fetch = [&](int j, uint32_t kofs) {
+  auto fetch = [&](int j, uint32_t ofs, bool v) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
     const size_t base = (size_t(k0) * p.hkv + kvh) * D;
-    ld.load_at(lds_addr(smem) + kofs, (rs ? p.k_recv : p.k_loc) + base, hi - k0);
-    ld.load_at(lds_addr(smem) + kofs + TILE, (rs ? p.v_recv : p.v_loc) + base, hi - k0);
+    const u16* src = v ? (rs ? p.v_recv : p.v_loc) : (rs ? p.k_recv : p.k_loc);
+    ld.load_at(lds_addr(smem) + ofs, src + base, hi - k0);
   };
 
-  if (n_t > 0) fetch(0, 0);
+  if (n_t > 0) {
+    fetch(0, 0, false);
+    fetch(0, 2 * TILE, true);
+  }
+  if (n_t > 1) fetch(1, TILE, false);
 
   bf16x8 qreg[KS];
   {
@@ -118,7 +125,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   // normalised O and the LSE of the keys seen so far, to o_out/lse_out
   // (final: bf16 O, plus fp32 O when o_out is non-null)
   auto write_out = [&](float* o_out, float* lse_out) {
-    const float tot = lsum + __shfl_xor(lsum, 32);
+    const float tot = sum_halves(lsum);
     const float inv = tot > 0.f ? 1.f / tot : 0.f;
     const float lse = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
     if (qvalid) {
@@ -148,7 +155,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   float lse_recv = -INFINITY;  // merged: the received partial's LSE
   auto switch_source = [&]() {
     if (MERGED) {
-      const float tot = lsum + __shfl_xor(lsum, 32);
+      const float tot = sum_halves(lsum);
       lse_recv = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
     }
     write_out(p.o_f32_recv, MERGED ? nullptr : p.lse_recv);
@@ -157,34 +164,26 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     m = -INFINITY;
     lsum = 0.f;
   };
-  wait_async();
-  __syncthreads();
 
-  auto step = [&](int j, auto buf) {
-    constexpr uint32_t KO = decltype(buf)::value * 2 * TILE, VO = KO + TILE;
-    if (j + 1 < n_t) fetch(j + 1, 2 * TILE - KO);
-    const bool rs = j < n_r;
-    const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
-    const int hi = rs ? r1 : l1;
-    if (PAIRED && j == n_r) switch_source();
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) pk[ks] = opaque(pk[ks]);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      pv[db][0] = opaque(pv[db][0]);
-      pv[db][1] = opaque(pv[db][1]);
-    }
-
-    // S^T = K Q^T, two independent accumulator chains (32 keys each)
-    f32x16 s[2] = {zero16(), zero16()};
+  // S^T = K Q^T for the K tile at byte offset ko (prologue only; the loop
+  // interleaves the same products with the softmax), two independent
+  // accumulator chains (32 keys each)
+  auto scores = [&](f32x16 (&s)[2], uint32_t ko) {
+    s[0] = zero16();
+    s[1] = zero16();
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
-        s[mb] = mfma32(lds_b128(smem, pk[ks], KO + mb * 64 * D), qreg[ks], s[mb]);
-    // mask keys past the range and, on diagonal tiles, keys after the query:
-    // element i of block mb is key k0 + 4*half + cst(mb, i), visible iff
-    // cst < rel (one compare per score)
+        s[mb] = mfma32(lds_b128(smem, pk[ks], ko + mb * 64 * D), qreg[ks], s[mb]);
+  };
+  // scores of tile j: keys past the range and, on diagonal tiles, keys after
+  // the query are masked (element i of block mb is key k0 + 4*half +
+  // cst(mb, i), visible iff cst < rel: one compare per score, edge tiles only)
+  auto mask = [&](f32x16 (&s)[2], int j) {
+    const bool rs = j < n_r;
+    const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
+    const int hi = rs ? r1 : l1;
     const bool diag = !rs && k0 >= ldiag;
     if (diag || k0 + BN > hi) {
       const int rel = (diag ? min(hi, qrow + 1) : hi) - k0 - 4 * half;
@@ -194,18 +193,54 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
         for (int i = 0; i < 16; ++i)
           s[mb][i] = mb * 32 + 8 * (i >> 2) + (i & 3) < rel ? s[mb][i] : -INFINITY;
     }
+  };
+  // row maximum of masked scores (scaled, log2 units)
+  auto row_max = [&](const f32x16 (&s)[2]) {
     float mx = -INFINITY;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[mb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
-    const bool grow = mx > m + kLazy;  // implies mx > m
+    return max_halves(mx) * c;
+  };
+
+  wait_async();
+  __syncthreads();
+  f32x16 sa[2], sb[2];  // scores of the current and of the next tile
+  float mxa = -INFINITY, mxb = -INFINITY;
+  if (n_t > 0) {
+    scores(sa, 0);
+    mask(sa, 0);
+    mxa = row_max(sa);
+  }
+
+  // Iteration j runs the online softmax of tile j (scores sc and row maximum
+  // mxc, both from the previous iteration) beside the MFMAs of tile j+1's
+  // scores into sn, then O^T += V^T P^T for tile j beside tile j+1's mask
+  // and row maximum (to mxn). The MFMAs form a fixed sequence of slots: a
+  // slot issues the LDS reads of the slot two ahead, its MFMA and its share
+  // of the vector work, then a scheduling barrier, so the softmax runs in
+  // the MFMAs' shadow. The last iteration computes the scores of a tile that
+  // does not exist (from whatever its K buffer holds: finite data or stale
+  // bits, never read past the buffer) and drops them; one iteration body,
+  // with no branch per slot and no second copy for the last tile.
+  constexpr int NS = 2 * KS + 4 * DB;  // score slots, then PV slots
+  constexpr int EX = 32 / (2 * KS);    // exponentials per score slot
+  constexpr int MX = 3;                // first PV slot that takes maxima
+  constexpr int MPS = (32 + (4 * DB - MX) - 1) / (4 * DB - MX);  // maxima per slot
+  auto step = [&](int j, auto par, f32x16 (&sc)[2], float mxc, f32x16 (&sn)[2], float& mxn) {
+    constexpr int PAR = decltype(par)::value;
+    constexpr uint32_t KN = (1 - PAR) * TILE, VC = (2 + PAR) * TILE;
+    if (j + 1 < n_t) fetch(j + 1, (3 - PAR) * TILE, true);   // V of tile j+1
+    if (j + 2 < n_t) fetch(j + 2, PAR * TILE, false);        // K of tile j+2
+    if (PAIRED && j == n_r) switch_source();
+    // a row's output is rescaled only when its maximum grows by more than
+    // the headroom; rows that do not grow keep their maximum and scale by 1
+    const bool grow = mxc > m + kLazy;  // implies mxc > m
     if (__any(grow)) {
-      // rows that do not grow keep their maximum and scale by exactly 1
       const float alpha =
-          !grow ? 1.f : m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mx);
-      m = grow ? mx : m;
+          !grow ? 1.f : m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mxc);
+      m = grow ? mxc : m;
       lsum *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
@@ -213,35 +248,71 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
         for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
     }
     const float mref = m == -INFINITY ? 0.f : m;
-    float ps = 0.f;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int ks = 0; ks < KS; ++ks) pk[ks] = opaque(pk[ks]);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], c, -mref));
-        s[mb][i] = e;
-        ps += e;
-      }
-    lsum += ps;
-
-    // O^T += V^T P^T, 16 keys per MFMA step
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const bf16x8 pb = pack8(s[kk >> 1], 8 * (kk & 1));
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const uint32_t ro = VO + kk * 32 * D;  // rows 16*kk..
-        oacc[db] = mfma32(cat8(lds_tr(smem, pv[db][0], ro), lds_tr(smem, pv[db][1], ro)), pb,
-                          oacc[db]);
-      }
+    for (int db = 0; db < DB; ++db) {
+      pv[db][0] = opaque(pv[db][0]);
+      pv[db][1] = opaque(pv[db][1]);
     }
-    __builtin_amdgcn_sched_barrier(0);  // keep this tile's MFMAs ahead of the wait
+
+    bf16x8 ring[3], pb[4];
+    // operand of slot n: K rows of tile j+1 (score slots), V^T of tile j
+    // (PV slots)
+    auto rd = [&](int n) {
+      if (n < 2 * KS) {
+        ring[n % 3] = lds_b128(smem, pk[n / 2], KN + (n % 2) * 64 * D);
+      } else {
+        const int u = n - 2 * KS, kk = u / DB, db = u % DB;
+        const uint32_t ro = VC + kk * 32 * D;  // rows 16*kk..
+        ring[n % 3] = cat8(lds_tr(smem, pv[db][0], ro), lds_tr(smem, pv[db][1], ro));
+      }
+    };
+    float ps = 0.f, mx = -INFINITY;
+    sn[0] = zero16();
+    sn[1] = zero16();
+    rd(0);
+    rd(1);
+    static_for<0, NS>([&](auto nc) {
+      constexpr int n = decltype(nc)::value;
+      if (n + 2 < NS) rd(n + 2);
+      if constexpr (n < 2 * KS) {
+        sn[n % 2] = mfma32(ring[n % 3], qreg[n / 2], sn[n % 2]);
+#pragma unroll
+        for (int e = n * EX; e < (n + 1) * EX; ++e) {
+          const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e / 16][e % 16], c, -mref));
+          sc[e / 16][e % 16] = x;
+          ps += x;
+          if (e % 8 == 7) {
+            pb[e / 8] = pack8(sc[e / 16], 8 * ((e / 8) & 1));
+            // complete here: keeps the exponentials in the score slots
+            // rather than sunk past the masking branch into the PV slots
+            asm volatile("" ::"v"(pb[e / 8]));
+          }
+        }
+        if (n == 2 * KS - 1) {
+          lsum += ps;
+          asm volatile("" : "+v"(lsum));  // the row sum too, not sunk into the next step
+        }
+      } else {
+        constexpr int u = n - 2 * KS;
+        oacc[u % DB] = mfma32(ring[n % 3], pb[u / DB], oacc[u % DB]);
+        if constexpr (u == MX - 1) mask(sn, j + 1);
+        if constexpr (u >= MX) {
+#pragma unroll
+          for (int e = (u - MX) * MPS; e < (u - MX + 1) * MPS && e < 32; ++e)
+            mx = fmaxf(mx, sn[e / 16][e % 16]);
+        }
+        if constexpr (u == 4 * DB - 1) mxn = max_halves(mx) * c;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
     wait_async();
     __syncthreads();
   };
   for (int j = 0; j < n_t; j += 2) {
-    step(j, std::integral_constant<int, 0>());
-    if (j + 1 < n_t) step(j + 1, std::integral_constant<int, 1>());
+    step(j, std::integral_constant<int, 0>(), sa, mxa, sb, mxb);
+    if (j + 1 < n_t) step(j + 1, std::integral_constant<int, 1>(), sb, mxb, sa, mxa);
   }
 
   if (PAIRED && n_r == n_t) switch_source();  // no local tile (never empty in practice)
@@ -249,21 +320,30 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     // local partial (registers) merged with the received one (workspace,
     // written by this lane at the switch; the waits since have completed it)
     wait_async();
-    const float tot = lsum + __shfl_xor(lsum, 32);
+    const float tot = sum_halves(lsum);
     const float inv = tot > 0.f ? 1.f / tot : 0.f;
     const float lse_loc = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
     const Merge2 w = merge2(lse_loc, lse_recv);
     if (qvalid) {
       const size_t ob = ((size_t)qrow * p.hq + h) * D;
+      // every read of the received partial is issued before the first store
+      // (the compiler cannot tell the buffers apart and would otherwise wait
+      // for each read in turn)
+      f32x4 y[DB][4];
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          y[db][g] = *reinterpret_cast<const f32x4*>(p.o_f32_recv + ob + 32 * db + 8 * g + 4 * half);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int dcol = 32 * db + 8 * g + 4 * half;
-          const f32x4 y = *reinterpret_cast<const f32x4*>(p.o_f32_recv + ob + dcol);
           f32x4 v;
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) v[jj] = merge2_value(w, oacc[db][4 * g + jj] * inv, y[jj]);
+          for (int jj = 0; jj < 4; ++jj)
+            v[jj] = merge2_value(w, oacc[db][4 * g + jj] * inv, y[db][g][jj]);
           uint2 packed;
           packed.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
           packed.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);

@@ -51,7 +51,7 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5;
   const int kvh = b % p.hkv;
-  const int item = p.perm[b / p.hkv];
+  const int item = b / p.hkv;  // the launch list is in launch order
   const int32_t* it = p.items + 8 * item;  // launch list
   const int k0 = it[0], k1 = it[1], q0 = it[2], q1 = it[3], qfull = it[4], src = it[5];
   const u16* Kg = src ? p.k_recv : p.k_loc;

@@ -45,7 +45,7 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
   const int kvh = b % p.hkv;
   const int rest = b / p.hkv;
   const int hc = rest % p.head_chunks;
-  const int32_t* it = p.items + 8 * p.perm[rest / p.head_chunks];
+  const int32_t* it = p.items + 8 * (rest / p.head_chunks);
   const int q0 = it[0], q1 = it[1], r0 = it[2], r1 = it[3], l0 = it[4], l1 = it[5];
   const int ldiag = it[6];
 

@@ -226,6 +226,22 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// Lane l combined with lane l ^ 32 (the other half of the wave) through
+// v_permlane32_swap, a VALU exchange with no LDS round trip: after the swap
+// one register holds x of lanes 0-31 in both halves and the other x of lanes
+// 32-63, so one max or add of the two gives each lane the pair's result
+// (addition commutes exactly, so the bits equal x + x[l ^ 32]).
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Index of this thread's wave in the workgroup, as a wave-uniform value.
 __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);

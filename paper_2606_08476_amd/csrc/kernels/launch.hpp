@@ -13,8 +13,7 @@ struct FwdParams {
   const uint16_t* v_recv;
   const uint16_t* k_loc;    // [t_q, hkv, d]
   const uint16_t* v_loc;
-  const int32_t* items;     // 8 int32 per item: q0 q1 r0 r1 l0 l1 ldiag seg
-  const int32_t* perm;      // launch order
+  const int32_t* items;     // 8 int32 per item, in launch order: q0 q1 r0 r1 l0 l1 ldiag seg
   int32_t n_items;
   int32_t hq, hkv, group, head_chunks;
   float scale_log2;         // softmax scale * log2(e)
@@ -41,8 +40,7 @@ struct BwdParams {
   const uint16_t* v_loc;
   const uint16_t* k_recv;
   const uint16_t* v_recv;
-  const int32_t* items;     // 8 int32 per item: k0 k1 q0 q1 qfull src seg slot
-  const int32_t* perm;
+  const int32_t* items;     // 8 int32 per item, in launch order: k0 k1 q0 q1 qfull src seg slot
   const int32_t* lim;       // [t_q] receive index end per query
   const int32_t* qfirst;    // per item, per 32-key wave: first query row that sees it
   float* part_k;            // [slots, hkv, 128, d] partial dK/dV of split key tiles
@@ -66,8 +64,7 @@ struct DqParams {
   const uint16_t* v_recv;
   const uint16_t* k_loc;
   const uint16_t* v_loc;
-  const int32_t* items;     // fused forward items: q0 q1 r0 r1 l0 l1 ldiag seg
-  const int32_t* perm;
+  const int32_t* items;     // fused forward items, in launch order: q0 q1 r0 r1 l0 l1 ldiag seg
   int32_t n_items;
   int32_t hq, hkv, group, head_chunks;
   float scale;
