@@ -82,12 +82,24 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   const int ntile = (q1 - q0 + BM - 1) / BM;
   const int n_it = ntile * p.group;
 
+  // iteration i covers query head kvh * group + i / ntile and query tile
+  // i % ntile; both are carried from one iteration to the next (no integer
+  // division per iteration)
+  int cur_t = 0;              // query tile of the current iteration
+  int nxt_t = 0, nxt_h = 0;   // query tile and head of the next copy
+  auto advance = [&]() {
+    if (++nxt_t == ntile) {
+      nxt_t = 0;
+      ++nxt_h;
+    }
+  };
+
   // next iteration: Q/dO tiles, LSE, D and receive limits, all copied from
   // HBM straight into LDS (rows past q1 repeat the last query; masked)
   const TileLoader<D, BM> ldq(p.hq * D);
-  auto fetch = [&](int i_, int buf) {
-    const int h = kvh * p.group + i_ / ntile;
-    const int t0 = q0 + (i_ % ntile) * BM;
+  auto fetch = [&](int hh, int tt, int buf) {
+    const int h = kvh * p.group + hh;
+    const int t0 = q0 + tt * BM;
     const size_t base = (size_t(t0) * p.hq + h) * D;
     const uint32_t sb = lds_addr(smem);
     ldq.load_at(sb + (buf ? OQ1 : OQ0), p.q + base, q1 - t0);
@@ -120,7 +132,8 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
   const int kx = kvalid ? kidx : 0x7fffffff;  // never below a receive limit
 
-  if (n_it > 0) fetch(0, 0);
+  if (n_it > 0) fetch(0, 0, 0);
+  advance();
   wait_async();
   __syncthreads();
 
@@ -234,8 +247,10 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   // where no row sees any of them (the tile ends before qfirst, or the keys
   // are past the range); masked otherwise.
   auto step = [&](int i_, auto bufc) {
-    const int t0 = q0 + (i_ % ntile) * BM;
-    if (i_ + 1 < n_it) fetch(i_ + 1, decltype(bufc)::value ^ 1);
+    const int t0 = q0 + cur_t * BM;
+    if (i_ + 1 < n_it) fetch(nxt_h, nxt_t, decltype(bufc)::value ^ 1);
+    cur_t = nxt_t;
+    advance();
     pr = opaque(pr);
     pt = opaque(pt);
     const int tlast = min(t0 + BM, q1) - 1;

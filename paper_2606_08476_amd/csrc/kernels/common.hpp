@@ -275,15 +275,18 @@ struct TileLoader {
   // the same with the tile's LDS byte address
   __device__ __forceinline__ void load_at(uint32_t tile, const u16* g, int nvalid) const {
     const uint32_t lds = tile + 1024u * wave_id();
+    if (nvalid >= ROWS) {  // uniform: a whole tile, the offsets as computed
 #pragma unroll
-    for (int u = 0; u < N; ++u) {
-      uint32_t o = off[u];
-      if (nvalid < ROWS) {  // uniform: only the last, ragged tile of a range
+      for (int u = 0; u < N; ++u) lds_copy16(g, off[u], lds + 16u * NT * u);
+    } else {  // the last, ragged tile of a range: a per-lane select, no branch
+#pragma unroll
+      for (int u = 0; u < N; ++u) {
         const int L = u * NT + threadIdx.x;
         const int r = L / CH;
-        if (r >= nvalid) o = 2u * uint32_t((nvalid - 1) * row_stride + 8 * ((L % CH) ^ swz<D>(r)));
+        const uint32_t alt =
+            2u * uint32_t((nvalid - 1) * row_stride + 8 * ((L % CH) ^ swz<D>(r)));
+        lds_copy16(g, r >= nvalid ? alt : off[u], lds + 16u * NT * u);
       }
-      lds_copy16(g, o, lds + 16u * NT * u);
     }
   }
 };
