@@ -92,6 +92,10 @@ SMALL = {
     # many one-token and short documents
     "short_docs": dict(workload="llama8b", cp=2, rank=1,
                        lens=[1, 1, 3, 1, 70, 1, 2, 129, 1, 64, 5, 250, 1, 31]),
+    # documents whose Per-Doc chunks are whole multiples of the 64-key and
+    # 128-key tiles: no ragged tile anywhere, masks exactly on tile edges
+    "aligned_docs": dict(workload="llama8b", cp=2, rank=0,
+                         lens=[512, 1024, 256, 2048, 512]),
 }
 
 
