@@ -101,15 +101,19 @@ def attention_fwd(cu, q_gpos, q, kv_gpos, k, v, scale=None, rows=None, dtype=tor
 
 def lse_merge(o_a, lse_a, o_b, lse_b):
     """Merge two partial results over disjoint key sets (O [T, H, d],
-    LSE [H, T]); a -inf LSE carries weight 0."""
+    LSE [H, T]); a -inf LSE carries weight 0, so a row that is empty in
+    both partials stays empty (O = 0, LSE = -inf), as a pass over the union
+    of the two key sets would leave it."""
     m = torch.maximum(lse_a, lse_b)
     m = torch.where(torch.isfinite(m), m, torch.zeros_like(m))
     wa = torch.exp(lse_a - m)
     wb = torch.exp(lse_b - m)
     tot = wa + wb
     lse = m + torch.log(tot)
-    ca = (wa / tot).T[:, :, None]
-    cb = (wb / tot).T[:, :, None]
+    some = tot > 0
+    safe = torch.where(some, tot, torch.ones_like(tot))
+    ca = torch.where(some, wa / safe, torch.zeros_like(wa)).T[:, :, None]
+    cb = torch.where(some, wb / safe, torch.zeros_like(wb)).T[:, :, None]
     return ca * o_a + cb * o_b, lse
 
 

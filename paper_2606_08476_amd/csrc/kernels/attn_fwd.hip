@@ -54,6 +54,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   // of tile j while the copies of K of tile j+2 and V of tile j+1 fill the
   // other two buffers. The loop is unrolled by two, so every read names its
   // buffer with a compile-time offset.
+  // Ordering rule: a buffer is refilled only after a barrier that follows
+  // every wave's last read of it. Iteration j refills K buffer j % 2, last
+  // read in iteration j-1 (before its closing barrier) -- or, for j = 0, in
+  // the prologue, which therefore ends with a barrier of its own.
   __shared__ __attribute__((aligned(16))) char smem[4 * TILE];
 
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -213,6 +217,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     mask(sa, 0);
     mxa = row_max(sa);
   }
+  // every wave has read K of tile 0 before iteration 0 copies tile 2 into
+  // the same buffer
+  if (n_t > 2) __syncthreads();
 
   // Iteration j runs the online softmax of tile j (scores sc and row maximum
   // mxc, both from the previous iteration) beside the MFMAs of tile j+1's

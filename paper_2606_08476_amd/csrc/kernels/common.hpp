@@ -293,8 +293,9 @@ struct TileLoader {
 
 // Log-sum-exp merge of two partial results over disjoint key sets (weights
 // of the partials and the merged LSE, natural log; a -inf partial has
-// weight 0). One definition for the merge kernel and the forward's merging
-// epilogue, so that both give the same bits.
+// weight 0, so two empty partials merge to O = 0, LSE = -inf). One
+// definition for the merge kernel and the forward's merging epilogue, so
+// that both give the same bits.
 struct Merge2 {
   float ca, cb, lse;
 };
@@ -303,7 +304,8 @@ __device__ __forceinline__ Merge2 merge2(float la, float lb) {
   const float m = mx == -INFINITY ? 0.f : mx;
   const float wa = __expf(la - m), wb = __expf(lb - m);
   const float tot = wa + wb;
-  return {wa / tot, wb / tot, m + __logf(tot)};
+  const bool any = tot > 0.f;
+  return {any ? wa / tot : 0.f, any ? wb / tot : 0.f, m + __logf(tot)};
 }
 __device__ __forceinline__ float merge2_value(const Merge2& w, float a, float b) {
   return __builtin_fmaf(w.ca, a, w.cb * b);

@@ -6,6 +6,7 @@ LSE |err| <= 1e-3 * max(1, |LSE|); the gather and every integer table are
 bit-exact. Partial passes must reproduce -inf LSE and zero O on rows that
 see no key of their source.
 """
+import math
 import sys
 
 import numpy as np
@@ -217,6 +218,32 @@ def test_partial_passes_and_merge(key, dev):
     F.fc_lse_merge(dv(Oa), dv(La), dv(Ob), dv(Lb), ob, of, lo)
     torch.cuda.synchronize()
     assert _maxabs(ob, Om) <= O_TOL and _maxabs(of, Om) <= 1e-5 and _lse_ok(lo, Lm) <= 1e-5
+
+
+def test_merge_of_empty_rows(dev):
+    """fc_lse_merge on rows where one or both partials are empty (LSE =
+    -inf, O = 0): a row empty in both stays empty (O = 0, LSE = -inf), any
+    other row takes the non-empty side; against the oracle's merge."""
+    t, h, d = 37, 3, 64
+    g = torch.Generator().manual_seed(5)
+    Oa, Ob = torch.randn(t, h, d, generator=g), torch.randn(t, h, d, generator=g)
+    La, Lb = torch.randn(h, t, generator=g) * 3, torch.randn(h, t, generator=g) * 3
+    sel = torch.rand(h, t, generator=g)
+    La[sel < 0.5] = -math.inf
+    Lb[(sel < 0.25) | (sel > 0.8)] = -math.inf
+    for L, O in ((La, Oa), (Lb, Ob)):
+        O.transpose(0, 1)[torch.isinf(L)] = 0
+    Om, Lm = A.lse_merge(Oa.double(), La.double(), Ob.double(), Lb.double())
+    dv = lambda x: x.contiguous().to(dev)
+    ob = torch.empty(t, h, d, dtype=torch.bfloat16, device=dev)
+    of = torch.empty(t, h, d, dtype=torch.float32, device=dev)
+    lo = torch.empty(h, t, dtype=torch.float32, device=dev)
+    F.fc_lse_merge(dv(Oa), dv(La), dv(Ob), dv(Lb), ob, of, lo)
+    torch.cuda.synchronize()
+    both = (torch.isinf(La) & torch.isinf(Lb))
+    assert both.any()
+    assert torch.isfinite(of).all() and torch.all(of.cpu().transpose(0, 1)[both] == 0)
+    assert _lse_ok(lo, Lm) <= 1e-5 and _maxabs(of, Om) <= 1e-5 and _maxabs(ob, Om) <= O_TOL
 
 
 @pytest.mark.parametrize("key", SMALL)

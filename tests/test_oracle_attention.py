@@ -170,6 +170,29 @@ def test_merge_of_arbitrary_split_equals_single_pass():
     assert torch.allclose(Om, O, atol=1e-13) and torch.allclose(Lm, L, atol=1e-13)
 
 
+def test_merge_of_two_empty_partials_is_empty():
+    """Rows that see no key of either partial (three key sets: the merge of
+    the first two is an empty partial for rows whose keys all lie in the
+    third) merge to O = 0, LSE = -inf, and merging that result with the
+    third partial gives the single pass."""
+    lens = [6, 5]
+    cu, q, k, v, _ = _packed(lens, 2, 1, 8, 12)
+    T = cu[-1]
+    ar = np.arange(T)
+    a, b, c = np.array([1]), np.array([2]), np.setdiff1d(ar, [1, 2])
+    Oa, La = A.attention_fwd(cu, ar, q, a, k[a], v[a], 0.3)
+    Ob, Lb = A.attention_fwd(cu, ar, q, b, k[b], v[b], 0.3)
+    Oab, Lab = A.lse_merge(Oa, La, Ob, Lb)
+    empty = torch.isinf(La) & torch.isinf(Lb)
+    assert empty.any() and (~empty).any()
+    assert torch.equal(torch.isinf(Lab), empty) and (Lab[empty] < 0).all()
+    assert torch.all(Oab.transpose(0, 1)[empty] == 0) and torch.isfinite(Oab).all()
+    Oc, Lc = A.attention_fwd(cu, ar, q, c, k[c], v[c], 0.3)
+    Om, Lm = A.lse_merge(Oab, Lab, Oc, Lc)
+    O, L = A.attention_fwd(cu, ar, q, ar, k, v, 0.3)
+    assert torch.allclose(Om, O, atol=1e-13) and torch.allclose(Lm, L, atol=1e-13)
+
+
 def test_empty_partial_pass():
     lens = [4, 4]
     cu, q, k, v, _ = _packed(lens, 2, 1, 8, 9)
