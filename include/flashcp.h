@@ -272,6 +272,23 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
                      const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
                      float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * fc_attn_bwd with the same arguments except the workspace, which comes
+ * from a library-owned static device array of FC_NOALLOC_SCRATCH_BYTES per
+ * GPU (held from module load until the process ends). Makes no device
+ * allocation. FC_ERR_WORKSPACE, before any launch, when the view's
+ * backward workspace (fc_workspace_size) exceeds that size; FC_ERR_INVALID_ARG
+ * when `stream` belongs to another device than the current one. Results
+ * are those of fc_attn_bwd. Every call on one GPU shares that GPU's array:
+ * calls whose work overlaps on the same GPU (other streams, other threads)
+ * race and must be serialised by the caller. */
+#define FC_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+int fc_attn_bwd_noalloc(fc_view view, const void* q, const void* k_loc, const void* v_loc,
+                        const void* k_recv, const void* v_recv, const void* o, const float* lse,
+                        const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
+                        float* dk_recv, float* dv_recv, void* stream);
+
 const char* fc_last_error(void);
 
 #ifdef __cplusplus

@@ -21,6 +21,7 @@ SOURCES = [
     "host/plan.cpp",
     "host/view.cpp",
     "host/api.cpp",
+    "host/noalloc.cpp",
     "kernels/attn_fwd.hip",
     "kernels/attn_bwd.hip",
     "kernels/attn_bwd_dq.hip",
@@ -51,7 +52,9 @@ def _hipcc() -> str:
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, src.replace("/", "_") + ".o")
     path = os.path.join(CSRC, src)
-    lang = ["-x", "hip"] if src.endswith(".hip") else ["-x", "hip"]
+    # every source is compiled as HIP: the host sources launch kernels or
+    # name device symbols
+    lang = ["-x", "hip"]
     cmd = [_hipcc(), *FLAGS, *lang, "-c", path, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:

@@ -30,8 +30,11 @@ EXPORTS = [
     "fc_plan_stats", "fc_view_create", "fc_view_get_info", "fc_view_export", "fc_view_bind",
     "fc_view_destroy", "fc_workspace_size", "fc_kv_gather", "fc_attn_fwd",
     "fc_attn_fwd_partial", "fc_attn_fwd_partials", "fc_lse_merge", "fc_attn_bwd", "fc_bwd_preprocess",
-    "fc_attn_bwd_pass", "fc_attn_bwd_dkdv", "fc_attn_bwd_dq", "fc_last_error",
+    "fc_attn_bwd_pass", "fc_attn_bwd_dkdv", "fc_attn_bwd_dq", "fc_attn_bwd_noalloc", "fc_last_error",
 ]
+
+# bytes of the static device scratch behind fc_attn_bwd_noalloc (flashcp.h)
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
 
 
 class FlashCPError(RuntimeError):
@@ -99,6 +102,7 @@ def lib():
             "fc_attn_bwd_pass": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P, C.c_size_t, P],
             "fc_attn_bwd_dkdv": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, C.c_size_t, P],
             "fc_attn_bwd_dq": [P, P, P, P, P, P, P, P, P, C.c_float, P, P],
+            "fc_attn_bwd_noalloc": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -366,6 +370,24 @@ def fc_attn_bwd(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale
         _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
         _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), ws.data_ptr(), ws.numel() * ws.element_size(),
         _stream()))
+
+
+def fc_attn_bwd_noalloc(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale,
+                        dq, dk_loc, dv_loc, dk_recv, dv_recv):
+    """fc_attn_bwd with its workspace in the library's static device scratch
+    (no device allocation)."""
+    import torch
+    i = view.info
+    bf, f32 = torch.bfloat16, torch.float32
+    tq, tr, hq, hkv, d = i["t_q"], i["t_recv"], i["hq"], i["hkv"], i["d"]
+    _check(lib().fc_attn_bwd_noalloc(
+        view.handle, _ptr(q, (tq, hq, d), bf, "q"), _ptr(k_loc, (tq, hkv, d), bf, "k_loc"),
+        _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
+        _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), _ptr(o, (tq, hq, d), bf, "o"),
+        _ptr(lse, (hq, tq), f32, "lse"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
+        _ptr(dq, (tq, hq, d), f32, "dq"), _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"),
+        _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
+        _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), _stream()))
 
 
 def fc_bwd_preprocess(view: View, o, dout, delta):
