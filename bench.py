@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama8b")
     ap.add_argument("--mode", choices=["two_pass"], default="two_pass")
+    ap.add_argument("--bwd", choices=["det", "atomic"], default="det",
+                    help="backward mode: deterministic (query-major dQ pass) or atomic "
+                         "(dQ added by the key-major pass)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle baseline sample (0 disables it)")
     ap.add_argument("--study", choices=["planner", "granularity"], default=None,
@@ -392,7 +395,7 @@ def main():
         ev[3].record()
         # dK/dV (key-major) and dQ (query-major) workgroups in one launch
         F.fc_attn_bwd_pass(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq, dk_loc,
-                           dv_loc, dk_recv, dv_recv, dkdv_ws)
+                           dv_loc, dk_recv, dv_recv, dkdv_ws, deterministic=args.bwd == "det")
         ev[4].record()
 
     for _ in range(args.warmup):

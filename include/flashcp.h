@@ -238,20 +238,29 @@ int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const f
                  int32_t t, int32_t h, int32_t d, void* o_bf16, float* o_f32, float* lse_out,
                  void* stream);
 
-/* Backward of the rank's attention, given the forward's o (bf16) and the
- * final (merged) lse, and dout. Writes dq (fp32 [T_q,Hq,d]), dk_loc/dv_loc
- * (fp32 [T_q,Hkv,d]) and dk_recv/dv_recv (fp32 [T_r,Hkv,d]); dK/dV are
- * summed over the query heads of each KV head. ws: device, >= bwd bytes.
- * No atomics: results are bitwise reproducible for fixed inputs. */
+/* Backward of the rank's attention (the gradient of the merged two-pass
+ * result is the softmax gradient with the merged LSE, Sec. 2.3), given the
+ * forward's o (bf16) and final lse, and dout. Writes dq (fp32 [T_q,Hq,d],
+ * 16-byte aligned), dk_loc/dv_loc (fp32 [T_q,Hkv,d]) and dk_recv/dv_recv
+ * (fp32 [T_r,Hkv,d]); dK/dV are summed over the query heads of each KV
+ * head. ws: device, >= bwd bytes of fc_workspace_size.
+ * deterministic != 0: no atomics anywhere, results bitwise reproducible for
+ * fixed inputs (a query-major pass recomputes S and dP for dQ).
+ * deterministic == 0: the key-major pass also adds dQ with fp32 atomics (no
+ * recompute); dK/dV are still reproducible, dQ's last bits vary from run to
+ * run with the order of the additions. */
 int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                 const void* k_recv, const void* v_recv, const void* o, const float* lse,
-                const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes, void* stream);
+                const void* dout, float scale, int32_t deterministic, float* dq,
+                float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv, void* ws,
+                size_t ws_bytes, void* stream);
 
 /* The backward in its two steps (fc_attn_bwd runs both):
  * fc_bwd_preprocess writes delta[h, t] = sum_i dout[t,h,i] * o[t,h,i] (fp32
  * [Hq,T_q], device); fc_attn_bwd_pass then computes dk_*, dv_* (key-major
- * kernel) and dq (query-major kernel) from lse and delta. */
+ * kernel) and dq from lse and delta: by a query-major kernel when
+ * deterministic != 0, else by atomics from the key-major kernel (dq is
+ * zeroed first, on the stream). */
 int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta,
                       void* stream);
 /* The two kernels of fc_attn_bwd_pass, callable alone: the key-major
@@ -269,8 +278,9 @@ int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v
                    const void* dout, float scale, float* dq, void* stream);
 int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,
-                     const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                     float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes, void* stream);
+                     const void* dout, float scale, int32_t deterministic, float* dq,
+                     float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv, void* ws,
+                     size_t ws_bytes, void* stream);
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc):
@@ -286,8 +296,9 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
 #define FC_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
 int fc_attn_bwd_noalloc(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                         const void* k_recv, const void* v_recv, const void* o, const float* lse,
-                        const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                        float* dk_recv, float* dv_recv, void* stream);
+                        const void* dout, float scale, int32_t deterministic, float* dq,
+                        float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv,
+                        void* stream);
 
 const char* fc_last_error(void);
 

@@ -151,6 +151,32 @@ int launch_reduce(const View& v, const fck::BwdParams& p, hipStream_t s) {
                     "attn_bwd reduce launch");
 }
 
+// The backward pass once delta is known (arguments validated by the
+// caller). Deterministic: dK/dV and dQ workgroups in one launch (dQ written
+// once by the workgroup owning its rows). Otherwise key tiles only, each
+// adding its share of dQ into `dq` with atomics; `dq` must be zero on
+// entry. Either way the split key tiles' partial dK/dV are then reduced.
+int run_pass(const View& v, const void* q, const void* k_loc, const void* v_loc,
+             const void* k_recv, const void* v_recv, const float* lse, const float* delta,
+             const void* dout, float scale, int32_t deterministic, float* dq, float* dk_loc,
+             float* dv_loc, float* dk_recv, float* dv_recv, void* ws, size_t need,
+             hipStream_t s) {
+  fck::BwdParams p = bwd_params(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
+                                dk_loc, dv_loc, dk_recv, dv_recv, ws, need);
+  if (deterministic) {
+    const fck::DqParams d = dq_params(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout,
+                                      scale, dq);
+    if (int rc = hip_status(fck::launch_bwd_grid(p, d, v.d, v.heads_per_tile, s),
+                            "attn_bwd launch"))
+      return rc;
+  } else {
+    p.dq = dq;
+    if (int rc = hip_status(fck::launch_bwd_atomic(p, v.d, s), "attn_bwd (atomic dQ) launch"))
+      return rc;
+  }
+  return launch_reduce(v, p, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -304,7 +330,7 @@ int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delt
   if (!o || !dout || !delta) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
   return hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o),
                                                static_cast<const uint16_t*>(dout), delta,
-                                               v->t_q(), v->hq, v->d,
+                                               v->t_q(), v->hq, v->d, nullptr,
                                                reinterpret_cast<hipStream_t>(stream)),
                     "bwd preprocess launch");
 }
@@ -349,8 +375,9 @@ int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v
 
 int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                      const void* k_recv, const void* v_recv, const float* lse, const float* delta,
-                     const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                     float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes, void* stream) {
+                     const void* dout, float scale, int32_t deterministic, float* dq,
+                     float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv, void* ws,
+                     size_t ws_bytes, void* stream) {
   fc::clear_error();
   View* v;
   if (int rc = check_view(view, v)) return rc;
@@ -358,26 +385,24 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
   if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dq || !dk_loc || !dv_loc ||
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  if (reinterpret_cast<uintptr_t>(dq) % 16) return fail(FC_ERR_INVALID_ARG, "dq must be 16-byte aligned");
   const size_t need = part_ws(*v);
   if (need && (!ws || ws_bytes < need))
     return fail(FC_ERR_WORKSPACE, "dK/dV workspace of " + std::to_string(ws_bytes) +
                                       " bytes, need " + std::to_string(need));
-  // dK/dV and dQ workgroups in one launch, then the reduce of split key tiles
-  const fck::BwdParams p = bwd_params(*v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout,
-                                      scale, dk_loc, dv_loc, dk_recv, dv_recv, ws, need);
-  const fck::DqParams d = dq_params(*v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout,
-                                    scale, dq);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (int rc = hip_status(fck::launch_bwd_grid(p, d, v->d, v->heads_per_tile, s),
-                          "attn_bwd launch"))
-    return rc;
-  return launch_reduce(*v, p, s);
+  if (!deterministic &&
+      hip_status(fck::launch_fill_zero(dq, int64_t(v->t_q()) * v->hq * v->d, s), "dq zero fill"))
+    return FC_ERR_HIP;
+  return run_pass(*v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, deterministic,
+                  dq, dk_loc, dv_loc, dk_recv, dv_recv, ws, need, s);
 }
 
 int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                 const void* k_recv, const void* v_recv, const void* o, const float* lse,
-                const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes, void* stream) {
+                const void* dout, float scale, int32_t deterministic, float* dq, float* dk_loc,
+                float* dv_loc, float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes,
+                void* stream) {
   fc::clear_error();
   View* v;
   if (int rc = check_view(view, v)) return rc;
@@ -386,17 +411,23 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
   if (!ws || ws_bytes < need)
     return fail(FC_ERR_WORKSPACE, "backward workspace of " + std::to_string(ws_bytes) +
                                       " bytes, need " + std::to_string(need));
-  if (!o) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  float* delta = static_cast<float*>(ws);
-  // validate the pass's arguments before the first launch
-  if (!q || !k_loc || !v_loc || !lse || !dout || !dq || !dk_loc || !dv_loc ||
+  if (!o || !q || !k_loc || !v_loc || !lse || !dout || !dq || !dk_loc || !dv_loc ||
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  if (int rc = fc_bwd_preprocess(view, o, dout, delta, stream)) return rc;
+  if (reinterpret_cast<uintptr_t>(dq) % 16) return fail(FC_ERR_INVALID_ARG, "dq must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  float* delta = static_cast<float*>(ws);
+  // the preprocess also zeroes dq for the atomic pass
+  if (int rc = hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o),
+                                                     static_cast<const uint16_t*>(dout), delta,
+                                                     v->t_q(), v->hq, v->d,
+                                                     deterministic ? nullptr : dq, s),
+                          "bwd preprocess launch"))
+    return rc;
   const size_t dbytes = delta_ws(*v);
-  return fc_attn_bwd_pass(view, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, dq,
-                          dk_loc, dv_loc, dk_recv, dv_recv, static_cast<char*>(ws) + dbytes,
-                          ws_bytes - dbytes, stream);
+  return run_pass(*v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale, deterministic,
+                  dq, dk_loc, dv_loc, dk_recv, dv_recv, static_cast<char*>(ws) + dbytes,
+                  part_ws(*v), s);
 }
 
 }  // extern "C"

@@ -18,6 +18,7 @@
 #include <mutex>
 
 #include "internal.hpp"
+#include "view.hpp"
 
 using fc::fail;
 
@@ -53,10 +54,13 @@ extern "C" {
 
 int fc_attn_bwd_noalloc(fc_view view, const void* q, const void* k_loc, const void* v_loc,
                         const void* k_recv, const void* v_recv, const void* o, const float* lse,
-                        const void* dout, float scale, float* dq, float* dk_loc, float* dv_loc,
-                        float* dk_recv, float* dv_recv, void* stream) {
+                        const void* dout, float scale, int32_t deterministic, float* dq,
+                        float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv,
+                        void* stream) {
   fc::clear_error();
   if (!view) return fail(FC_ERR_INVALID_ARG, "view is null");
+  if (!reinterpret_cast<const fc::View*>(view)->dev_meta)
+    return fail(FC_ERR_WORKSPACE, "view is not bound to device metadata");
   size_t need = 0;
   if (int rc = fc_workspace_size(view, FC_TWO_PASS, nullptr, &need, nullptr)) return rc;
   if (need > kScratchBytes)
@@ -79,8 +83,8 @@ int fc_attn_bwd_noalloc(fc_view view, const void* q, const void* k_loc, const vo
   }
   void* ws = nullptr;
   if (int rc = scratch_address(dev, &ws)) return rc;
-  return fc_attn_bwd(view, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale, dq, dk_loc,
-                     dv_loc, dk_recv, dv_recv, ws, kScratchBytes, stream);
+  return fc_attn_bwd(view, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale, deterministic,
+                     dq, dk_loc, dv_loc, dk_recv, dv_recv, ws, kScratchBytes, stream);
 }
 
 }  // extern "C"

@@ -17,6 +17,16 @@
 // Masking (edge tiles only): local keys are causal in local order; a
 // received key is seen by a query iff its index is below the query's
 // receive limit.
+//
+// With DQ (the non-deterministic backward), the same workgroup also adds
+// this key tile's share of dQ = scale dS K into dQ: each wave writes its dS
+// block, transposed, into an LDS tile of all 128 keys (dS holds a key per
+// lane here; the dQ product needs the keys along the contraction), and after
+// a barrier wave w computes dQ for the query tile's 32 rows and head-dim
+// columns 32w..32w+31 (MFMA, dS and K both read from LDS with transpose
+// reads) and adds it into dQ with fp32 atomics. No second pass recomputes S
+// and dP; the order of the additions into dQ, and so its last bits, varies
+// from run to run.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -24,14 +34,16 @@
 
 namespace fck {
 
-template <int D>
+template <int D, bool DQ = false>
 struct DkdvLds {
-  static constexpr uint32_t bytes = 6 * 256 + (128 + 4 * 32) * D * 2;
+  // LSE/delta/limit slots, the key tile, two Q and two dO tiles; with DQ the
+  // transposed dS tile (128 keys x 32 queries, bf16) after them
+  static constexpr uint32_t bytes = 6 * 256 + (128 + 4 * 32) * D * 2 + (DQ ? 128 * 32 * 2 : 0);
 };
 
-// One workgroup's key tile (workgroup index b); smem: DkdvLds<D>::bytes of
-// shared memory.
-template <int D>
+// One workgroup's key tile (workgroup index b); smem: DkdvLds<D, DQ>::bytes
+// of shared memory.
+template <int D, bool DQ = false>
 __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem) {
   constexpr int BN = 128;       // keys per workgroup
   constexpr int BM = 32;        // queries per iteration
@@ -46,7 +58,13 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   // offset (all below 64 KiB, the reach of the offset field).
   constexpr uint32_t OK = 6 * 256;
   constexpr uint32_t OQ0 = OK + KT, OO0 = OQ0 + QT, OQ1 = OO0 + QT, OO1 = OQ1 + QT;
-  static_assert(OO1 + QT == DkdvLds<D>::bytes, "LDS layout");
+  // dS^T tile (DQ only): row k (key) holds the tile's 32 queries, 64 bytes;
+  // the 8-byte chunk c (queries 4c..4c+3) of row k sits at chunk position
+  // c ^ ((k >> 2) & 7), so that the row writes of a wave (32 keys, one
+  // chunk) and the transpose reads (4 keys x 16 queries per 16 lanes) both
+  // spread over the 64 banks
+  constexpr uint32_t ODS = OO1 + QT;
+  static_assert(ODS + (DQ ? 128 * 32 * 2 : 0) == DkdvLds<D, DQ>::bytes, "LDS layout");
 
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5;
@@ -85,7 +103,7 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   // iteration i covers query head kvh * group + i / ntile and query tile
   // i % ntile; both are carried from one iteration to the next (no integer
   // division per iteration)
-  int cur_t = 0;              // query tile of the current iteration
+  int cur_t = 0, cur_h = 0;   // query tile and head of the current iteration
   int nxt_t = 0, nxt_h = 0;   // query tile and head of the next copy
   auto advance = [&]() {
     if (++nxt_t == ntile) {
@@ -149,6 +167,19 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   constexpr int EP = 16 / KS, ES = 8 / DB;  // P / dS elements per slot
   // The compute of one query tile; P is masked (a branch after its last
   // slot) only on edge tiles.
+  // DQ: store this wave's dS block (bf16; w0 holds queries 4h..4h+3 and
+  // 8+4h..8+4h+3 of this lane's key, w1 the same plus 16) as rows of the
+  // dS^T tile: four 8-byte chunk writes per lane
+  // (the lane-derived addresses of the dQ stage are recomputed from an
+  // opaque copy of the lane index, not hoisted and held across the loop)
+  auto put_ds = [&](const uint4& w0, const uint4& w1) {
+    const uint32_t krow = 32 * wave + (opaque(uint32_t(lane)) & 31);
+    const uint32_t row = ODS + krow * 64, sw = (krow >> 2) & 7;
+    *reinterpret_cast<uint2*>(smem + row + 8 * (uint32_t(half) ^ sw)) = make_uint2(w0.x, w0.y);
+    *reinterpret_cast<uint2*>(smem + row + 8 * ((2u + half) ^ sw)) = make_uint2(w0.z, w0.w);
+    *reinterpret_cast<uint2*>(smem + row + 8 * ((4u + half) ^ sw)) = make_uint2(w1.x, w1.y);
+    *reinterpret_cast<uint2*>(smem + row + 8 * ((6u + half) ^ sw)) = make_uint2(w1.z, w1.w);
+  };
   auto tile = [&](int t0, auto bufc, bool edge) {
     constexpr int B = decltype(bufc)::value;
     constexpr uint32_t QO = B ? OQ1 : OQ0, OO = B ? OO1 : OO0, SO = 768u * B;
@@ -236,9 +267,84 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
       } else {
         const int u = n - 2 * KS - 2 * DB, kh = u / DB, db = u % DB;
         dk[db] = mfma32(sa[kh], a, dk[db]);
+        if constexpr (DQ) {
+          if (u == 0) put_ds(__builtin_bit_cast(uint4, sa[0]), __builtin_bit_cast(uint4, sa[1]));
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     });
+  };
+
+  // DQ: after a barrier (every wave's dS rows are in the dS^T tile), wave w
+  // computes dQ for the iteration's 32 query rows and head-dim columns
+  // 32w..32w+31 over the tile's 128 keys, and adds it into dQ. Operands by
+  // transpose reads: A (dS, 32 queries x 16 keys per k-step s) from the
+  // dS^T tile -- lane 32h + 16g + t reads rows 16s + 4h + t/4 (then + 8),
+  // chunk 4g + t%4, whose swizzle is (4s + h) & 7 (then (4s + 2 + h) & 7):
+  // the base below XOR 32*(s & 1) (and XOR 16) -- and B (K, 16 keys x 32
+  // columns) from the key tile, as the Q/dO tiles are read for dV and dK.
+  // With D = 64 there are two column blocks; waves 2 and 3 take the second
+  // half of the keys for them (two partial sums per column block).
+  constexpr int KPARTS = 4 / DB;         // key parts of the dQ product
+  constexpr int QSTEPS = 8 / KPARTS;     // 16-key steps per wave
+  auto dq_part = [&](f32x16& qacc) {
+    __syncthreads();
+    const int cb = wave % DB, kpart = wave / DB;
+    const uint32_t ln = opaque(uint32_t(lane));
+    const int t = ln & 15, g = (ln >> 4) & 1, hf = ln >> 5;
+    // (a key part starts at a multiple of 64 rows: its offset leaves the
+    // low bits the XORs act on untouched)
+    const uint32_t a0 = uint32_t((4 * hf + (t >> 2)) * 64 + 8 * ((4 * g + (t & 3)) ^ hf)) +
+                        uint32_t(kpart) * QSTEPS * 1024u;
+    const uint32_t kofs_q = uint32_t(kpart) * QSTEPS * 32u * D;
+    const uint32_t b0 = (pt ^ uint32_t(cb << 6)) + kofs_q;
+    const uint32_t b1 = (pt ^ uint32_t((cb << 6) | 32)) + 16 * D + kofs_q;
+    qacc = zero16();
+    // operands of k-step j into ring entry j % 3, two steps ahead of the
+    // MFMA that uses them (QSTEPS is even, so the parity of j is that of the
+    // k-step)
+    bf16x8 ra[3], rb[3];
+    auto rdq = [&](int j) {
+      const uint32_t x = 32u * uint32_t(j & 1);
+      ra[j % 3] = cat8(lds_tr(smem, a0 ^ x, ODS + 1024u * j),
+                       lds_tr(smem, a0 ^ x ^ 16u, ODS + 1024u * j + 512u));
+      rb[j % 3] = cat8(lds_tr(smem, b0, OK + uint32_t(j) * 32u * D),
+                       lds_tr(smem, b1, OK + uint32_t(j) * 32u * D));
+    };
+    rdq(0);
+    rdq(1);
+    static_for<0, QSTEPS>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      if (j + 2 < QSTEPS) rdq(j + 2);
+      qacc = mfma32(ra[j % 3], rb[j % 3], qacc);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+  // DQ: add the iteration's dQ block into dQ. Issued after the iteration's
+  // closing wait and barrier, so the atomics complete while the next
+  // iteration computes (its closing vmcnt(0) wait, which also covers them,
+  // comes an iteration later) instead of stalling this one.
+  auto dq_add = [&](int t0, int hh, const f32x16& qacc) {
+    const int cb = wave % DB;
+    const uint32_t ln = opaque(uint32_t(lane));
+    const int hf = ln >> 5;
+    // C layout: register i is query row 8*(i/4) + 4h + i%4, column 32cb +
+    // lane%32; each register's 64 lanes cover two 128-byte row segments.
+    // Addresses: a wave-uniform row base per register (scalar registers)
+    // plus one 32-bit lane offset shared by all sixteen.
+    // (the stride goes through an empty asm per iteration, so the row bases
+    // are recomputed here by scalar arithmetic rather than kept, sixteen
+    // 64-bit values, across the loop)
+    uint32_t rs = uint32_t(p.hq) * D;
+    asm volatile("" : "+s"(rs));
+    const uint32_t loff = uint32_t(4 * hf) * rs + 32u * cb + (ln & 31);
+    float* const base = p.dq + (size_t(t0) * p.hq + kvh * p.group + hh) * D;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r0 = 8 * (i >> 2) + (i & 3);
+      float* const bi = base + size_t(r0) * rs;
+      if (t0 + r0 + 4 * hf < q1) atomicAdd(bi + loff, p.scale * qacc[i]);
+    }
   };
   // One pipelined iteration: start the next tile's copies, compute this one,
   // wait for the copies. Each wave picks its own variant of the compute:
@@ -247,17 +353,24 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   // where no row sees any of them (the tile ends before qfirst, or the keys
   // are past the range); masked otherwise.
   auto step = [&](int i_, auto bufc) {
-    const int t0 = q0 + cur_t * BM;
+    const int t0 = q0 + cur_t * BM, hh = cur_h;
     if (i_ + 1 < n_it) fetch(nxt_h, nxt_t, decltype(bufc)::value ^ 1);
     cur_t = nxt_t;
+    cur_h = nxt_h;
     advance();
     pr = opaque(pr);
     pt = opaque(pt);
     const int tlast = min(t0 + BM, q1) - 1;
-    if (!(kw >= k1 || tlast < qfirst))
-      tile(t0, bufc, !(t0 >= qfull && t0 + BM <= q1 && kw + 32 <= k1));
+    const bool computed = !(kw >= k1 || tlast < qfirst);
+    if (computed) tile(t0, bufc, !(t0 >= qfull && t0 + BM <= q1 && kw + 32 <= k1));
+    f32x16 qacc;
+    if constexpr (DQ) {
+      if (!computed) put_ds(uint4{0u, 0u, 0u, 0u}, uint4{0u, 0u, 0u, 0u});
+      dq_part(qacc);
+    }
     wait_async();
     __syncthreads();
+    if constexpr (DQ) dq_add(t0, hh, qacc);
   };
   for (int i_ = 0; i_ < n_it; i_ += 2) {
     step(i_, std::integral_constant<int, 0>());

@@ -1,5 +1,6 @@
 // Bandwidth-bound kernels: the KV gather (simulated receive), the
-// log-sum-exp merge of two partial passes, and the backward preprocess.
+// log-sum-exp merge of two partial passes, the backward preprocess (which
+// can zero the atomic backward's dQ in the same pass), and a zero fill.
 // Each moves whole rows with 16-byte accesses, consecutive lanes on
 // consecutive addresses.
 #include "common.hpp"
@@ -58,16 +59,23 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const float* __restrict_
   if (c == 0) lse_out[li] = w.lse;
 }
 
-// delta[head, tok] = sum_d dO * O over one (token, head) row.
+// delta[head, tok] = sum_d dO * O over one (token, head) row; with dq_zero,
+// the same row of that fp32 tensor is zeroed too.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(const u16* __restrict__ o,
                                                       const u16* __restrict__ dout,
-                                                      float* delta, int32_t t, int32_t h) {
+                                                      float* delta, int32_t t, int32_t h,
+                                                      float* dq_zero) {
   constexpr int LPR = D / 8;  // lanes per row, 8 values each
   const int64_t row = (int64_t(blockIdx.x) * 256 + threadIdx.x) / LPR;
   const int c = threadIdx.x % LPR;
   const bool ok = row < int64_t(t) * h;
   float acc = 0.f;
+  if (ok && dq_zero) {
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    reinterpret_cast<f32x4*>(dq_zero + row * D)[2 * c] = z;
+    reinterpret_cast<f32x4*>(dq_zero + row * D)[2 * c + 1] = z;
+  }
   if (ok) {
     const uint4 a = reinterpret_cast<const uint4*>(o + row * D)[c];
     const uint4 g = reinterpret_cast<const uint4*>(dout + row * D)[c];
@@ -118,6 +126,13 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const int32_t* __restri
     reinterpret_cast<f32x4*>(dk + g)[c] = ak;
     reinterpret_cast<f32x4*>(dv + g)[c] = av;
   }
+}
+
+// x[0 .. n) = 0 (n a multiple of 4; x 16-byte aligned)
+__global__ __launch_bounds__(256) void fill_zero_kernel(f32x4* x, int64_t n4) {
+  const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n4; i += int64_t(gridDim.x) * 256)
+    x[i] = z;
 }
 
 static unsigned grid_for(int64_t threads) {
@@ -176,17 +191,27 @@ hipError_t launch_bwd_reduce(const int32_t* entries, int32_t n, const float* par
 }
 
 hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta,
-                                 int32_t t, int32_t h, int32_t d, hipStream_t s) {
+                                 int32_t t, int32_t h, int32_t d, float* dq_zero, hipStream_t s) {
   const int64_t rows = int64_t(t) * h;
   if (rows == 0) return hipSuccess;
   if (d == 64)
     hipLaunchKernelGGL(bwd_pre_kernel<64>, dim3(grid_for(rows * 8)), dim3(256), 0, s, o, dout,
-                       delta, t, h);
+                       delta, t, h, dq_zero);
   else if (d == 128)
     hipLaunchKernelGGL(bwd_pre_kernel<128>, dim3(grid_for(rows * 16)), dim3(256), 0, s, o, dout,
-                       delta, t, h);
+                       delta, t, h, dq_zero);
   else
     return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float* x, int64_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (n % 4 || reinterpret_cast<uintptr_t>(x) % 16) return hipErrorInvalidValue;
+  int64_t blocks = (n / 4 + 255) / 256;
+  if (blocks > 256 * 32) blocks = 256 * 32;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned(blocks)), dim3(256), 0, s,
+                     reinterpret_cast<f32x4*>(x), n / 4);
   return hipGetLastError();
 }
 

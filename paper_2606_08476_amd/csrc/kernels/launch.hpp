@@ -53,6 +53,7 @@ struct BwdParams {
   float* dk_recv;           // [t_r, hkv, d] fp32
   float* dv_recv;
   int32_t t_q;
+  float* dq;                // [t_q, hq, d] fp32, added into (atomic pass only)
 };
 
 struct DqParams {
@@ -76,14 +77,19 @@ hipError_t launch_fwd(const FwdParams& p, int d, int heads_per_tile, bool final_
                       hipStream_t s);
 hipError_t launch_bwd_dq(const DqParams& p, int d, int heads_per_tile, hipStream_t s);
 hipError_t launch_bwd(const BwdParams& p, int d, hipStream_t s);
+// dK/dV with dQ added into p.dq by atomics (p.dq zeroed beforehand)
+hipError_t launch_bwd_atomic(const BwdParams& p, int d, hipStream_t s);
 // dK/dV and dQ in one launch (dK/dV workgroups first)
 hipError_t launch_bwd_grid(const BwdParams& bp, const DqParams& dp, int d, int heads_per_tile,
                            hipStream_t s);
 hipError_t launch_bwd_reduce(const int32_t* entries, int32_t n, const float* part_k,
                              const float* part_v, int32_t hkv, int32_t d, float* dk_loc,
                              float* dv_loc, float* dk_recv, float* dv_recv, hipStream_t s);
+// delta = rowsum(dout * o); with a non-null dq_zero, also zeroes that
+// [t, h, d] fp32 tensor (the atomic backward's dQ) in the same pass
 hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta,
-                                 int32_t t, int32_t h, int32_t d, hipStream_t s);
+                                 int32_t t, int32_t h, int32_t d, float* dq_zero, hipStream_t s);
+hipError_t launch_fill_zero(float* x, int64_t n, hipStream_t s);
 hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o_b,
                             const float* lse_b, int32_t t, int32_t h, int32_t d, uint16_t* o_bf16,
                             float* o_f32, float* lse_out, hipStream_t s);

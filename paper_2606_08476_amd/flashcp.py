@@ -97,12 +97,15 @@ def lib():
             "fc_attn_fwd_partial": [P, C.c_int32, P, P, P, C.c_float, P, P, P],
             "fc_attn_fwd_partials": [P, P, P, P, P, P, C.c_float, P, P, P, P, P],
             "fc_lse_merge": [P, P, P, P, C.c_int32, C.c_int32, C.c_int32, P, P, P, P],
-            "fc_attn_bwd": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P, C.c_size_t, P],
+            "fc_attn_bwd": [P, P, P, P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, P, P,
+                            C.c_size_t, P],
             "fc_bwd_preprocess": [P, P, P, P, P],
-            "fc_attn_bwd_pass": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P, C.c_size_t, P],
+            "fc_attn_bwd_pass": [P, P, P, P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, P, P,
+                                 C.c_size_t, P],
             "fc_attn_bwd_dkdv": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, C.c_size_t, P],
             "fc_attn_bwd_dq": [P, P, P, P, P, P, P, P, P, C.c_float, P, P],
-            "fc_attn_bwd_noalloc": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, P],
+            "fc_attn_bwd_noalloc": [P, P, P, P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, P,
+                                    P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -356,7 +359,7 @@ def fc_lse_merge(o_a, lse_a, o_b, lse_b, o_bf16, o_f32, lse_out):
 
 
 def fc_attn_bwd(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale,
-                dq, dk_loc, dv_loc, dk_recv, dv_recv, ws):
+                dq, dk_loc, dv_loc, dk_recv, dv_recv, ws, deterministic: bool = True):
     import torch
     i = view.info
     bf, f32 = torch.bfloat16, torch.float32
@@ -366,6 +369,7 @@ def fc_attn_bwd(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale
         _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
         _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), _ptr(o, (tq, hq, d), bf, "o"),
         _ptr(lse, (hq, tq), f32, "lse"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
+        int(bool(deterministic)),
         _ptr(dq, (tq, hq, d), f32, "dq"), _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"),
         _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
         _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), ws.data_ptr(), ws.numel() * ws.element_size(),
@@ -373,7 +377,7 @@ def fc_attn_bwd(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale
 
 
 def fc_attn_bwd_noalloc(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale,
-                        dq, dk_loc, dv_loc, dk_recv, dv_recv):
+                        dq, dk_loc, dv_loc, dk_recv, dv_recv, deterministic: bool = True):
     """fc_attn_bwd with its workspace in the library's static device scratch
     (no device allocation)."""
     import torch
@@ -385,6 +389,7 @@ def fc_attn_bwd_noalloc(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dou
         _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
         _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), _ptr(o, (tq, hq, d), bf, "o"),
         _ptr(lse, (hq, tq), f32, "lse"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
+        int(bool(deterministic)),
         _ptr(dq, (tq, hq, d), f32, "dq"), _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"),
         _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
         _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), _stream()))
@@ -406,7 +411,7 @@ def _ws(ws):
 
 
 def fc_attn_bwd_pass(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, dout, scale,
-                     dq, dk_loc, dv_loc, dk_recv, dv_recv, ws=None):
+                     dq, dk_loc, dv_loc, dk_recv, dv_recv, ws=None, deterministic: bool = True):
     import torch
     i = view.info
     bf, f32 = torch.bfloat16, torch.float32
@@ -416,6 +421,7 @@ def fc_attn_bwd_pass(view: View, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do
         _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
         _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), _ptr(lse, (hq, tq), f32, "lse"),
         _ptr(delta, (hq, tq), f32, "delta"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
+        int(bool(deterministic)),
         _ptr(dq, (tq, hq, d), f32, "dq"), _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"),
         _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
         _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), *_ws(ws), _stream()))

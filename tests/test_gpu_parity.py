@@ -96,11 +96,21 @@ class Run:
         return A.attention_fwd(c.cu, o.q_gpos, x["q"], kv, k, v, rows=rows)
 
     def oracle_bwd(self, rows=None):
+        if rows is None and getattr(self, "_bwd_ref", None) is not None:
+            return self._bwd_ref
         c, o, x = self.case, self.case.oview, self.x
         kv = np.concatenate([o.q_gpos, o.recv_gpos])
         k = torch.cat([x["k_loc"], x["k_recv"]])
         v = torch.cat([x["v_loc"], x["v_recv"]])
-        return A.attention_bwd(c.cu, o.q_gpos, x["q"], kv, k, v, x["do"], rows=rows)
+        ref = A.attention_bwd(c.cu, o.q_gpos, x["q"], kv, k, v, x["do"], rows=rows)
+        if rows is None:
+            self._bwd_ref = ref
+        return ref
+
+    def bwd_outputs(self):
+        """NaN-filled dq, dk_loc, dv_loc, dk_recv, dv_recv like this run's."""
+        return [torch.full_like(t, float("nan")) for t in
+                (self.dq, self.dk_loc, self.dv_loc, self.dk_recv, self.dv_recv)]
 
 
 _RUNS = {}
@@ -255,6 +265,43 @@ def test_backward(key, dev):
              dk_recv=_maxabs(r.dk_recv, dk[tq:]), dv_recv=_maxabs(r.dv_recv, dv[tq:]))
     say(f"[gpu] {key} bwd: " + " ".join(f"{k} {v:.3e}" for k, v in e.items()))
     assert max(e.values()) <= G_TOL, e
+
+
+# dQ of the atomic backward against the deterministic one: the same dS
+# values summed in another order (fp32)
+DQ_ORDER_TOL = 1e-4
+
+
+@pytest.mark.parametrize("key", SMALL)
+def test_backward_atomic(key, dev):
+    """The non-deterministic backward (dQ added by the key-major pass with
+    atomics): dK/dV bit-identical to the deterministic backward, dQ within
+    the parity bound of the oracle and within fp32 reordering of the
+    deterministic dQ; through fc_attn_bwd (preprocess zeroes dQ) and
+    fc_attn_bwd_pass (zero fill of its own)."""
+    r = get_run(key, dev)
+    _, bws, pws = r.v.workspace_size()
+    ws = torch.empty(bws, dtype=torch.uint8, device=dev)
+    a = r.bwd_outputs()
+    F.fc_attn_bwd(r.v, r.q, r.k_loc, r.v_loc, r.k_recv, r.v_recv, r.o, r.lse, r.do, 0.0, *a, ws,
+                  deterministic=False)
+    delta = torch.empty_like(r.lse)
+    F.fc_bwd_preprocess(r.v, r.o, r.do, delta)
+    b = r.bwd_outputs()
+    pws_t = torch.empty(max(pws, 1), dtype=torch.uint8, device=dev)
+    F.fc_attn_bwd_pass(r.v, r.q, r.k_loc, r.v_loc, r.k_recv, r.v_recv, r.lse, delta, r.do, 0.0,
+                       *b, pws_t, deterministic=False)
+    torch.cuda.synchronize()
+    det = (r.dq, r.dk_loc, r.dv_loc, r.dk_recv, r.dv_recv)
+    for outs in (a, b):
+        for name, x, y in zip(("dk_loc", "dv_loc", "dk_recv", "dv_recv"), outs[1:], det[1:]):
+            assert torch.equal(x, y), name
+        assert torch.isfinite(outs[0]).all()
+    e_order = max(_maxabs(a[0], r.dq.cpu()), _maxabs(b[0], r.dq.cpu()))
+    dq_ref, _, _ = r.oracle_bwd()
+    e_ref = max(_maxabs(a[0], dq_ref), _maxabs(b[0], dq_ref))
+    say(f"[gpu] {key} bwd atomic: dQ vs oracle {e_ref:.3e}, vs deterministic {e_order:.3e}")
+    assert e_ref <= G_TOL and e_order <= DQ_ORDER_TOL
 
 
 def test_document_isolation_on_gpu(dev):
