@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--bwd", choices=["det", "atomic"], default="det",
                     help="backward mode: deterministic (query-major dQ pass) or atomic "
                          "(dQ added by the key-major pass)")
+    ap.add_argument("--delta-from", choices=["f32", "bf16"], default="f32",
+                    help="output the backward preprocess reads: the forward's fp32 O (also "
+                         "written by the forward) or its bf16 O")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle baseline sample (0 disables it)")
     ap.add_argument("--study", choices=["planner", "granularity"], default=None,
@@ -274,6 +277,7 @@ def study_granularity(args):
                 kl, vl = e(tq, hkv, d, dt=bf), e(tq, hkv, d, dt=bf)
                 kr, vr = e(tr, hkv, d, dt=bf), e(tr, hkv, d, dt=bf)
                 o, lse, delta = e(tq, hq, d, dt=bf), e(hq, tq), e(hq, tq)
+                o32 = e(tq, hq, d)
                 dq, dkl, dvl = e(tq, hq, d), e(tq, hkv, d), e(tq, hkv, d)
                 dkr, dvr = e(tr, hkv, d), e(tr, hkv, d)
                 ws = torch.empty(max(v.workspace_size()[2], 1), dtype=torch.uint8, device=dev)
@@ -282,8 +286,8 @@ def study_granularity(args):
 
                 def run():
                     F.fc_kv_gather(v, k_pk, v_pk, kl, vl, kr, vr)
-                    F.fc_attn_fwd(v, q, kl, vl, kr, vr, 0.0, F.FC_TWO_PASS, o, None, lse, fws)
-                    F.fc_bwd_preprocess(v, o, do, delta)
+                    F.fc_attn_fwd(v, q, kl, vl, kr, vr, 0.0, F.FC_TWO_PASS, o, o32, lse, fws)
+                    F.fc_bwd_preprocess(v, o, do, delta, o_f32=o32)
                     F.fc_attn_bwd_pass(v, q, kl, vl, kr, vr, lse, delta, do, 0.0, dq, dkl, dvl, dkr, dvr, ws)
 
                 for _ in range(2):
@@ -364,6 +368,7 @@ def main():
     k_recv = torch.empty(tr, hkv, d, dtype=bf, device=dev)
     v_recv = torch.empty_like(k_recv)
     o = torch.empty(tq, hq, d, dtype=bf, device=dev)
+    o32 = torch.empty(tq, hq, d, dtype=f32, device=dev) if args.delta_from == "f32" else None
     lse = torch.empty(hq, tq, dtype=f32, device=dev)
     delta = torch.empty(hq, tq, dtype=f32, device=dev)
     dq = torch.empty(tq, hq, d, dtype=f32, device=dev)
@@ -389,9 +394,11 @@ def main():
         # both partial passes (received keys, then local keys) and their
         # log-sum-exp merge in one launch; with no received KV the local pass
         # alone writes the final O and LSE
-        F.fc_attn_fwd(v, q, k_loc, v_loc, k_recv, v_recv, 0.0, F.FC_TWO_PASS, o, None, lse, fwd_ws)
+        F.fc_attn_fwd(v, q, k_loc, v_loc, k_recv, v_recv, 0.0, F.FC_TWO_PASS, o, o32, lse, fwd_ws)
         ev[2].record()
-        F.fc_bwd_preprocess(v, o, do, delta)
+        # delta = rowsum(dO * O) from the fp32 O (exact to fp32; from the bf16
+        # O its rounding reaches every dS of the row)
+        F.fc_bwd_preprocess(v, o, do, delta, o_f32=o32)
         ev[3].record()
         # dK/dV (key-major) and dQ (query-major) workgroups in one launch
         F.fc_attn_bwd_pass(v, q, k_loc, v_loc, k_recv, v_recv, lse, delta, do, 0.0, dq, dk_loc,
@@ -450,7 +457,8 @@ def main():
         "kv_gather": ("hbm", 2 * 2 * kv_rows * hkv * d * 2),
         # both partial passes (4d per pair) with the merge in their epilogue
         "attn_fwd": ("mfma", 4.0 * d * hq * pairs),
-        "bwd_preprocess": ("hbm", tq * hq * (2 * 2 * d + 4)),
+        # dO (bf16) and O (fp32, or bf16) read, delta written
+        "bwd_preprocess": ("hbm", tq * hq * (2 * d + (4 if o32 is not None else 2) * d + 4)),
         # backward, algorithmic: S recomputed once, dP, dV, dK, dQ (10d per
         # pair, the FlashAttention count); the kernels execute 14d (the dQ
         # workgroups recompute S and dP), reported apart as executed_tflops

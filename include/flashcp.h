@@ -240,7 +240,11 @@ int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const f
 
 /* Backward of the rank's attention (the gradient of the merged two-pass
  * result is the softmax gradient with the merged LSE, Sec. 2.3), given the
- * forward's o (bf16) and final lse, and dout. Writes dq (fp32 [T_q,Hq,d],
+ * forward's output and final lse, and dout. The output is o (bf16) or, when
+ * o_f32 (fp32 [T_q,Hq,d], 16-byte aligned, nullable) is given, o_f32 (o is
+ * then not read and may be NULL): delta = rowsum(dout * O) from the fp32 O
+ * is exact to fp32 rounding, from the bf16 O it carries O's rounding into
+ * every dS of the row. Writes dq (fp32 [T_q,Hq,d],
  * 16-byte aligned), dk_loc/dv_loc (fp32 [T_q,Hkv,d]) and dk_recv/dv_recv
  * (fp32 [T_r,Hkv,d]); dK/dV are summed over the query heads of each KV
  * head. ws: device, >= bwd bytes of fc_workspace_size.
@@ -250,19 +254,20 @@ int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const f
  * recompute); dK/dV are still reproducible, dQ's last bits vary from run to
  * run with the order of the additions. */
 int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
-                const void* k_recv, const void* v_recv, const void* o, const float* lse,
-                const void* dout, float scale, int32_t deterministic, float* dq,
-                float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv, void* ws,
-                size_t ws_bytes, void* stream);
+                const void* k_recv, const void* v_recv, const void* o, const float* o_f32,
+                const float* lse, const void* dout, float scale, int32_t deterministic,
+                float* dq, float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv,
+                void* ws, size_t ws_bytes, void* stream);
 
 /* The backward in its two steps (fc_attn_bwd runs both):
- * fc_bwd_preprocess writes delta[h, t] = sum_i dout[t,h,i] * o[t,h,i] (fp32
- * [Hq,T_q], device); fc_attn_bwd_pass then computes dk_*, dv_* (key-major
+ * fc_bwd_preprocess writes delta[h, t] = sum_i dout[t,h,i] * O[t,h,i] (fp32
+ * [Hq,T_q], device), O being o_f32 when non-null, else the bf16 o;
+ * fc_attn_bwd_pass then computes dk_*, dv_* (key-major
  * kernel) and dq from lse and delta: by a query-major kernel when
  * deterministic != 0, else by atomics from the key-major kernel (dq is
  * zeroed first, on the stream). */
-int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta,
-                      void* stream);
+int fc_bwd_preprocess(fc_view view, const void* o, const float* o_f32, const void* dout,
+                      float* delta, void* stream);
 /* The two kernels of fc_attn_bwd_pass, callable alone: the key-major
  * dK/dV pass (writes dk_*, dv_*) and the query-major dQ pass (writes dq).
  * Key tiles seen by very many query tiles are split across workgroups that
@@ -295,8 +300,9 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
  * race and must be serialised by the caller. */
 #define FC_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
 int fc_attn_bwd_noalloc(fc_view view, const void* q, const void* k_loc, const void* v_loc,
-                        const void* k_recv, const void* v_recv, const void* o, const float* lse,
-                        const void* dout, float scale, int32_t deterministic, float* dq,
+                        const void* k_recv, const void* v_recv, const void* o,
+                        const float* o_f32, const float* lse, const void* dout, float scale,
+                        int32_t deterministic, float* dq,
                         float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv,
                         void* stream);
 

@@ -63,14 +63,25 @@ def _blocks(cu, q_gpos, kv_gpos, rows):
             yield r, ksel, torch.from_numpy(mask)
 
 
-def attention_fwd(cu, q_gpos, q, kv_gpos, k, v, scale=None, rows=None, dtype=torch.float64):
+def _heads(Hq, G, kv_heads):
+    """Query heads to compute: all, or those of the given KV heads."""
+    if kv_heads is None:
+        return list(range(Hq))
+    return [h for h in range(Hq) if h // G in set(int(j) for j in kv_heads)]
+
+
+def attention_fwd(cu, q_gpos, q, kv_gpos, k, v, scale=None, rows=None, dtype=torch.float64,
+                  kv_heads=None):
     """O [Tq, Hq, d] and LSE [Hq, Tq] of queries at ``q_gpos`` over the keys at
     ``kv_gpos`` (a partial pass whenever those keys are a subset of what the
     queries could see). ``rows`` restricts the computation to some queries;
-    other rows are returned as NaN."""
+    other rows are returned as NaN. ``kv_heads`` restricts it to the query
+    heads of those KV heads (each head is computed on its own, so the values
+    are those of the unrestricted call); other heads are NaN."""
     Tq, Hq, d = q.shape
     Hkv = k.shape[1]
     G = Hq // Hkv
+    heads = _heads(Hq, G, kv_heads)
     scale = 1.0 / math.sqrt(d) if scale is None or scale <= 0 else float(scale)
     q = q.to(dtype)
     k = k.to(dtype)
@@ -78,12 +89,13 @@ def attention_fwd(cu, q_gpos, q, kv_gpos, k, v, scale=None, rows=None, dtype=tor
     O = torch.full((Tq, Hq, d), float("nan"), dtype=dtype)
     LSE = torch.full((Hq, Tq), float("nan"), dtype=dtype)
     rows_all = np.arange(Tq) if rows is None else np.asarray(rows, dtype=np.int64)
-    O[rows_all] = 0
-    LSE[:, rows_all] = -math.inf
+    ht = torch.as_tensor(heads, dtype=torch.long)
+    O[rows_all[:, None], ht[None, :]] = 0
+    LSE[ht[:, None], rows_all[None, :]] = -math.inf
     for r, ks, mask in _blocks(cu, q_gpos, kv_gpos, rows):
         if ks.size == 0:
             continue
-        for h in range(Hq):
+        for h in heads:
             j = h // G
             s = scale * (q[r, h] @ k[ks, j].T)
             s = s.masked_fill(~mask, -math.inf)
@@ -117,7 +129,8 @@ def lse_merge(o_a, lse_a, o_b, lse_b):
     return ca * o_a + cb * o_b, lse
 
 
-def attention_bwd(cu, q_gpos, q, kv_gpos, k, v, do, scale=None, rows=None, dtype=torch.float64):
+def attention_bwd(cu, q_gpos, q, kv_gpos, k, v, do, scale=None, rows=None, dtype=torch.float64,
+                  kv_heads=None, with_fwd=False):
     """dQ [Tq, Hq, d], dK and dV [Tk, Hkv, d] of the full (single-pass)
     attention of queries at ``q_gpos`` over keys at ``kv_gpos``. The key set
     must contain every key the queries see, so the softmax is complete.
@@ -125,12 +138,17 @@ def attention_bwd(cu, q_gpos, q, kv_gpos, k, v, do, scale=None, rows=None, dtype
     ``rows`` restricts the backward to some queries: dQ is then computed for
     those rows only (others are zero) and dK/dV hold only their
     contributions, which is the exact gradient for every key that no other
-    query sees (e.g. all keys of a document whose queries are all in rows)."""
+    query sees (e.g. all keys of a document whose queries are all in rows).
+    ``kv_heads`` restricts it to those KV heads and their query heads (dQ of
+    other heads, dK/dV of other KV heads are NaN). With ``with_fwd`` the
+    forward's O and LSE are returned too, as (dQ, dK, dV, O, LSE)."""
     Tq, Hq, d = q.shape
     Tk, Hkv, _ = k.shape
     G = Hq // Hkv
+    heads = _heads(Hq, G, kv_heads)
     scale = 1.0 / math.sqrt(d) if scale is None or scale <= 0 else float(scale)
-    O, LSE = attention_fwd(cu, q_gpos, q, kv_gpos, k, v, scale, rows=rows, dtype=dtype)
+    O, LSE = attention_fwd(cu, q_gpos, q, kv_gpos, k, v, scale, rows=rows, dtype=dtype,
+                           kv_heads=kv_heads)
     q = q.to(dtype)
     k = k.to(dtype)
     v = v.to(dtype)
@@ -139,11 +157,17 @@ def attention_bwd(cu, q_gpos, q, kv_gpos, k, v, do, scale=None, rows=None, dtype
     dq = torch.zeros((Tq, Hq, d), dtype=dtype)
     dk = torch.zeros((Tk, Hkv, d), dtype=dtype)
     dv = torch.zeros((Tk, Hkv, d), dtype=dtype)
+    if kv_heads is not None:
+        other = [h for h in range(Hq) if h not in heads]
+        dq[:, other] = float("nan")
+        okv = [j for j in range(Hkv) if j not in set(int(x) for x in kv_heads)]
+        dk[:, okv] = float("nan")
+        dv[:, okv] = float("nan")
     for r, ks, mask in _blocks(cu, q_gpos, kv_gpos, rows):
         if ks.size == 0:
             continue
         kt = torch.from_numpy(ks)
-        for h in range(Hq):
+        for h in heads:
             j = h // G
             s = (scale * (q[r, h] @ k[ks, j].T)).masked_fill(~mask, -math.inf)
             p = torch.exp(s - LSE[h, r][:, None])
@@ -152,6 +176,8 @@ def attention_bwd(cu, q_gpos, q, kv_gpos, k, v, do, scale=None, rows=None, dtype
             dq[r, h] += scale * (ds @ k[ks, j])
             dk[:, j].index_add_(0, kt, scale * (ds.T @ q[r, h]))
             dv[:, j].index_add_(0, kt, p.T @ do[r, h])
+    if with_fwd:
+        return dq, dk, dv, O, LSE
     return dq, dk, dv
 
 

@@ -321,14 +321,16 @@ int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const f
                     "lse_merge launch");
 }
 
-int fc_bwd_preprocess(fc_view view, const void* o, const void* dout, float* delta,
-                      void* stream) {
+int fc_bwd_preprocess(fc_view view, const void* o, const float* o_f32, const void* dout,
+                      float* delta, void* stream) {
   fc::clear_error();
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
-  if (!o || !dout || !delta) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  return hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o),
+  if ((!o && !o_f32) || !dout || !delta) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
+  if (o_f32 && reinterpret_cast<uintptr_t>(o_f32) % 16)
+    return fail(FC_ERR_INVALID_ARG, "o_f32 must be 16-byte aligned");
+  return hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o), o_f32,
                                                static_cast<const uint16_t*>(dout), delta,
                                                v->t_q(), v->hq, v->d, nullptr,
                                                reinterpret_cast<hipStream_t>(stream)),
@@ -399,10 +401,10 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
 }
 
 int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_loc,
-                const void* k_recv, const void* v_recv, const void* o, const float* lse,
-                const void* dout, float scale, int32_t deterministic, float* dq, float* dk_loc,
-                float* dv_loc, float* dk_recv, float* dv_recv, void* ws, size_t ws_bytes,
-                void* stream) {
+                const void* k_recv, const void* v_recv, const void* o, const float* o_f32,
+                const float* lse, const void* dout, float scale, int32_t deterministic, float* dq,
+                float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv, void* ws,
+                size_t ws_bytes, void* stream) {
   fc::clear_error();
   View* v;
   if (int rc = check_view(view, v)) return rc;
@@ -411,14 +413,16 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
   if (!ws || ws_bytes < need)
     return fail(FC_ERR_WORKSPACE, "backward workspace of " + std::to_string(ws_bytes) +
                                       " bytes, need " + std::to_string(need));
-  if (!o || !q || !k_loc || !v_loc || !lse || !dout || !dq || !dk_loc || !dv_loc ||
+  if ((!o && !o_f32) || !q || !k_loc || !v_loc || !lse || !dout || !dq || !dk_loc || !dv_loc ||
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
   if (reinterpret_cast<uintptr_t>(dq) % 16) return fail(FC_ERR_INVALID_ARG, "dq must be 16-byte aligned");
+  if (o_f32 && reinterpret_cast<uintptr_t>(o_f32) % 16)
+    return fail(FC_ERR_INVALID_ARG, "o_f32 must be 16-byte aligned");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   float* delta = static_cast<float*>(ws);
   // the preprocess also zeroes dq for the atomic pass
-  if (int rc = hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o),
+  if (int rc = hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o), o_f32,
                                                      static_cast<const uint16_t*>(dout), delta,
                                                      v->t_q(), v->hq, v->d,
                                                      deterministic ? nullptr : dq, s),

@@ -53,8 +53,9 @@ int scratch_address(int dev, void** out) {
 extern "C" {
 
 int fc_attn_bwd_noalloc(fc_view view, const void* q, const void* k_loc, const void* v_loc,
-                        const void* k_recv, const void* v_recv, const void* o, const float* lse,
-                        const void* dout, float scale, int32_t deterministic, float* dq,
+                        const void* k_recv, const void* v_recv, const void* o,
+                        const float* o_f32, const float* lse, const void* dout, float scale,
+                        int32_t deterministic, float* dq,
                         float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv,
                         void* stream) {
   fc::clear_error();
@@ -83,7 +84,8 @@ int fc_attn_bwd_noalloc(fc_view view, const void* q, const void* k_loc, const vo
   }
   void* ws = nullptr;
   if (int rc = scratch_address(dev, &ws)) return rc;
-  return fc_attn_bwd(view, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale, deterministic,
+  return fc_attn_bwd(view, q, k_loc, v_loc, k_recv, v_recv, o, o_f32, lse, dout, scale,
+                     deterministic,
                      dq, dk_loc, dv_loc, dk_recv, dv_recv, ws, kScratchBytes, stream);
 }
 

@@ -148,7 +148,6 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   const bool kfull = k1 - k0 == BN;
   const float sl2 = p.scale * kLog2e;
   // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
-  const int kx = kvalid ? kidx : 0x7fffffff;  // never below a receive limit
 
   if (n_it > 0) fetch(0, 0, 0);
   advance();
@@ -187,15 +186,58 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
     // (register 4g + j): rows cq < hiq exist; on a local diagonal the key is
     // seen by rows cq >= lo; on a received diagonal by rows whose receive
     // limit exceeds the key index
+    // (this lane's key is recomputed here from an opaque lane index rather
+    // than held across the loop)
     const bool diag = t0 < qfull;
-    const int hiq = q1 - t0 - 4 * half;
-    const int lo = !kvalid ? 0x40000000 : (diag && !src) ? kidx - t0 - 4 * half : -0x40000000;
-    const int kl = (diag && src) ? kx : -0x7fffffff;
+    const uint32_t ln = opaque(uint32_t(lane));
+    const int hf = int(ln >> 5);
+    const int kid = k0 + 32 * wave + int(ln & 31);
+    const bool kval = kid < k1;
+    const int hiq = q1 - t0 - 4 * hf;
+    const int lo = !kval ? 0x40000000 : (diag && !src) ? kid - t0 - 4 * hf : -0x40000000;
+    const int kl = (diag && src) ? (kval ? kid : 0x7fffffff) : -0x7fffffff;
 
     f32x16 sacc = zero16(), dpacc = zero16();
     bf16x8 ra[3], rb[3], pa[2], sa[2];
+    // Where P is large (short documents, keys near the diagonal) the bf16
+    // rounding of P and dS dominates the dV/dK error. On a wave's tile with
+    // any P above 1/16 (rare on long documents) the bf16 residuals of P and
+    // dS also go through the dV and dK products: after the last dV slot,
+    // where P and the whole dS are still in fp32 registers, one branch forms
+    // both residuals and multiplies them by their operands (read again) into
+    // the same accumulators. Elsewhere each rounding error is at most 2^-13
+    // of a term.
+    constexpr float kSplitP = 1.0f / 16.0f;
+    bool split = false;
+    auto residual = [&](const bf16x8 (&lo)[2], uint32_t base, f32x16 (&acc)[DB]) {
+      static_for<0, 2 * DB>([&](auto uc) {
+        constexpr int u = decltype(uc)::value, kh = u / DB, db = u % DB;
+        const uint32_t t0_ = pt ^ (db << 6), t1_ = (pt ^ ((db << 6) | 32)) + 16 * D;
+        const bf16x8 b = cat8(lds_tr(smem, t0_, base + kh * 32 * D),
+                              lds_tr(smem, t1_, base + kh * 32 * D));
+        acc[db] = mfma32(lo[kh], b, acc[db]);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
     f32x4 l4[4], d4[4];
-    int4 m4[4];
+    // P = 0 where the key is not seen: keys past the range, later keys on a
+    // local diagonal, keys at or past a row's receive limit on a received
+    // diagonal (edge tiles only)
+    auto mask_p = [&](f32x16& pv) {
+      int4 m4[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        m4[g] = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int g = e >> 2, j = e & 3, cq = 8 * g + j;
+        // (local tiles never copy limits into LDS: what is there is stale
+        // and must not be compared)
+        const int lim = !src ? 0x7fffffff
+                        : j == 0 ? m4[g].x : j == 1 ? m4[g].y : j == 2 ? m4[g].z : m4[g].w;
+        pv[e] = ((cq >= lo) & (cq < hiq) & (kl < lim)) ? pv[e] : 0.f;
+      }
+    };
     // LDS operand reads of slot n into ring entry n % 3
     auto rd = [&](int n) {
       bf16x8& a = ra[n % 3];
@@ -240,21 +282,14 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
         if ((n - KS + 1) * EP == 8) pa[0] = pack8(sacc, 0);
         if (n == 2 * KS - 1) {
           if (edge) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-              m4[g] = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int g = e >> 2, j = e & 3, cq = 8 * g + j;
-              // (local tiles never copy limits into LDS: what is there is
-              // stale and must not be compared)
-              const int lim = !src ? 0x7fffffff
-                              : j == 0 ? m4[g].x : j == 1 ? m4[g].y : j == 2 ? m4[g].z : m4[g].w;
-              sacc[e] = ((cq >= lo) & (cq < hiq) & (kl < lim)) ? sacc[e] : 0.f;
-            }
+            mask_p(sacc);
             pa[0] = pack8(sacc, 0);
           }
           pa[1] = pack8(sacc, 8);
+          float pmax = sacc[0];
+#pragma unroll
+          for (int e = 1; e < 16; ++e) pmax = fmaxf(pmax, sacc[e]);
+          split = __any(pmax > kSplitP);
         }
       } else if (n < 2 * KS + 2 * DB) {
         const int u = n - 2 * KS, kh = u / DB, db = u % DB;
@@ -264,6 +299,10 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
           dpacc[e] = sacc[e] * (dpacc[e] - d4[e >> 2][e & 3]);
         if ((u + 1) * ES == 8) sa[0] = pack8(dpacc, 0);
         if ((u + 1) * ES == 16) sa[1] = pack8(dpacc, 8);
+        if (u == 2 * DB - 1 && split) {
+          residual({pack8_lo(sacc, 0), pack8_lo(sacc, 8)}, OO, dv);
+          residual({pack8_lo(dpacc, 0), pack8_lo(dpacc, 8)}, QO, dk);
+        }
       } else {
         const int u = n - 2 * KS - 2 * DB, kh = u / DB, db = u % DB;
         dk[db] = mfma32(sa[kh], a, dk[db]);

@@ -108,6 +108,17 @@ __device__ __forceinline__ bf16x8 pack8(const f32x16& c, int i0) {
   return r;
 }
 
+// The bf16 residuals of the same 8 values: c - bf16(c), rounded to bf16.
+// With pack8 it splits each value into a high and a low bf16 part whose sum
+// carries about 16 significant bits (a product taken over both parts is as
+// exact as its fp32 accumulation).
+__device__ __forceinline__ bf16x8 pack8_lo(const f32x16& c, int i0) {
+  bf16x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = (__bf16)(c[i0 + j] - (float)(__bf16)c[i0 + j]);
+  return r;
+}
+
 template <int D>
 __device__ __forceinline__ int swz(int r) {
   if constexpr (D == 128)

@@ -59,10 +59,11 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const float* __restrict_
   if (c == 0) lse_out[li] = w.lse;
 }
 
-// delta[head, tok] = sum_d dO * O over one (token, head) row; with dq_zero,
-// the same row of that fp32 tensor is zeroed too.
-template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(const u16* __restrict__ o,
+// delta[head, tok] = sum_d dO * O over one (token, head) row, from the bf16
+// O or (OF32) the fp32 O; with dq_zero, the same row of that fp32 tensor is
+// zeroed too.
+template <int D, bool OF32>
+__global__ __launch_bounds__(256) void bwd_pre_kernel(const void* __restrict__ o_,
                                                       const u16* __restrict__ dout,
                                                       float* delta, int32_t t, int32_t h,
                                                       float* dq_zero) {
@@ -77,13 +78,25 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const u16* __restrict__ o,
     reinterpret_cast<f32x4*>(dq_zero + row * D)[2 * c + 1] = z;
   }
   if (ok) {
-    const uint4 a = reinterpret_cast<const uint4*>(o + row * D)[c];
     const uint4 g = reinterpret_cast<const uint4*>(dout + row * D)[c];
-    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, gw[4] = {g.x, g.y, g.z, g.w};
+    const uint32_t gw[4] = {g.x, g.y, g.z, g.w};
+    if constexpr (OF32) {
+      const f32x4* op = reinterpret_cast<const f32x4*>(static_cast<const float*>(o_) + row * D);
+      const f32x4 a0 = op[2 * c], a1 = op[2 * c + 1];
+      const float av[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      acc += bf2f(u16(aw[j] & 0xffff)) * bf2f(u16(gw[j] & 0xffff));
-      acc += bf2f(u16(aw[j] >> 16)) * bf2f(u16(gw[j] >> 16));
+      for (int j = 0; j < 4; ++j) {
+        acc += av[2 * j] * bf2f(u16(gw[j] & 0xffff));
+        acc += av[2 * j + 1] * bf2f(u16(gw[j] >> 16));
+      }
+    } else {
+      const uint4 a = reinterpret_cast<const uint4*>(static_cast<const u16*>(o_) + row * D)[c];
+      const uint32_t aw[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        acc += bf2f(u16(aw[j] & 0xffff)) * bf2f(u16(gw[j] & 0xffff));
+        acc += bf2f(u16(aw[j] >> 16)) * bf2f(u16(gw[j] >> 16));
+      }
     }
   }
 #pragma unroll
@@ -190,16 +203,27 @@ hipError_t launch_bwd_reduce(const int32_t* entries, int32_t n, const float* par
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta,
-                                 int32_t t, int32_t h, int32_t d, float* dq_zero, hipStream_t s) {
+template <int D>
+static void launch_pre_d(const uint16_t* o, const float* o_f32, const uint16_t* dout,
+                         float* delta, int32_t t, int32_t h, float* dq_zero, hipStream_t s) {
   const int64_t rows = int64_t(t) * h;
-  if (rows == 0) return hipSuccess;
+  const dim3 grid(grid_for(rows * (D / 8))), block(256);
+  if (o_f32)
+    hipLaunchKernelGGL((bwd_pre_kernel<D, true>), grid, block, 0, s, o_f32, dout, delta, t, h,
+                       dq_zero);
+  else
+    hipLaunchKernelGGL((bwd_pre_kernel<D, false>), grid, block, 0, s, o, dout, delta, t, h,
+                       dq_zero);
+}
+
+hipError_t launch_bwd_preprocess(const uint16_t* o, const float* o_f32, const uint16_t* dout,
+                                 float* delta, int32_t t, int32_t h, int32_t d, float* dq_zero,
+                                 hipStream_t s) {
+  if (int64_t(t) * h == 0) return hipSuccess;
   if (d == 64)
-    hipLaunchKernelGGL(bwd_pre_kernel<64>, dim3(grid_for(rows * 8)), dim3(256), 0, s, o, dout,
-                       delta, t, h, dq_zero);
+    launch_pre_d<64>(o, o_f32, dout, delta, t, h, dq_zero, s);
   else if (d == 128)
-    hipLaunchKernelGGL(bwd_pre_kernel<128>, dim3(grid_for(rows * 16)), dim3(256), 0, s, o, dout,
-                       delta, t, h, dq_zero);
+    launch_pre_d<128>(o, o_f32, dout, delta, t, h, dq_zero, s);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -85,10 +85,12 @@ hipError_t launch_bwd_grid(const BwdParams& bp, const DqParams& dp, int d, int h
 hipError_t launch_bwd_reduce(const int32_t* entries, int32_t n, const float* part_k,
                              const float* part_v, int32_t hkv, int32_t d, float* dk_loc,
                              float* dv_loc, float* dk_recv, float* dv_recv, hipStream_t s);
-// delta = rowsum(dout * o); with a non-null dq_zero, also zeroes that
-// [t, h, d] fp32 tensor (the atomic backward's dQ) in the same pass
-hipError_t launch_bwd_preprocess(const uint16_t* o, const uint16_t* dout, float* delta,
-                                 int32_t t, int32_t h, int32_t d, float* dq_zero, hipStream_t s);
+// delta = rowsum(dout * o), o the fp32 o_f32 when non-null, else the bf16
+// o; with a non-null dq_zero, also zeroes that [t, h, d] fp32 tensor (the
+// atomic backward's dQ) in the same pass
+hipError_t launch_bwd_preprocess(const uint16_t* o, const float* o_f32, const uint16_t* dout,
+                                 float* delta, int32_t t, int32_t h, int32_t d, float* dq_zero,
+                                 hipStream_t s);
 hipError_t launch_fill_zero(float* x, int64_t n, hipStream_t s);
 hipError_t launch_lse_merge(const float* o_a, const float* lse_a, const float* o_b,
                             const float* lse_b, int32_t t, int32_t h, int32_t d, uint16_t* o_bf16,

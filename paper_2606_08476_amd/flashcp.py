@@ -97,15 +97,15 @@ def lib():
             "fc_attn_fwd_partial": [P, C.c_int32, P, P, P, C.c_float, P, P, P],
             "fc_attn_fwd_partials": [P, P, P, P, P, P, C.c_float, P, P, P, P, P],
             "fc_lse_merge": [P, P, P, P, C.c_int32, C.c_int32, C.c_int32, P, P, P, P],
-            "fc_attn_bwd": [P, P, P, P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, P, P,
+            "fc_attn_bwd": [P, P, P, P, P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, P, P,
                             C.c_size_t, P],
-            "fc_bwd_preprocess": [P, P, P, P, P],
+            "fc_bwd_preprocess": [P, P, P, P, P, P],
             "fc_attn_bwd_pass": [P, P, P, P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, P, P,
                                  C.c_size_t, P],
             "fc_attn_bwd_dkdv": [P, P, P, P, P, P, P, P, P, C.c_float, P, P, P, P, P, C.c_size_t, P],
             "fc_attn_bwd_dq": [P, P, P, P, P, P, P, P, P, C.c_float, P, P],
-            "fc_attn_bwd_noalloc": [P, P, P, P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P, P,
-                                    P],
+            "fc_attn_bwd_noalloc": [P, P, P, P, P, P, P, P, P, P, C.c_float, C.c_int32, P, P, P, P,
+                                    P, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -359,7 +359,9 @@ def fc_lse_merge(o_a, lse_a, o_b, lse_b, o_bf16, o_f32, lse_out):
 
 
 def fc_attn_bwd(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale,
-                dq, dk_loc, dv_loc, dk_recv, dv_recv, ws, deterministic: bool = True):
+                dq, dk_loc, dv_loc, dk_recv, dv_recv, ws, deterministic: bool = True, o_f32=None):
+    """o: the forward's bf16 output; o_f32 (optional): its fp32 output, from
+    which delta is then computed (o may be None)."""
     import torch
     i = view.info
     bf, f32 = torch.bfloat16, torch.float32
@@ -368,7 +370,7 @@ def fc_attn_bwd(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale
         view.handle, _ptr(q, (tq, hq, d), bf, "q"), _ptr(k_loc, (tq, hkv, d), bf, "k_loc"),
         _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
         _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), _ptr(o, (tq, hq, d), bf, "o"),
-        _ptr(lse, (hq, tq), f32, "lse"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
+        _ptr(o_f32, (tq, hq, d), f32, "o_f32"), _ptr(lse, (hq, tq), f32, "lse"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
         int(bool(deterministic)),
         _ptr(dq, (tq, hq, d), f32, "dq"), _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"),
         _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
@@ -377,7 +379,8 @@ def fc_attn_bwd(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale
 
 
 def fc_attn_bwd_noalloc(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dout, scale,
-                        dq, dk_loc, dv_loc, dk_recv, dv_recv, deterministic: bool = True):
+                        dq, dk_loc, dv_loc, dk_recv, dv_recv, deterministic: bool = True,
+                        o_f32=None):
     """fc_attn_bwd with its workspace in the library's static device scratch
     (no device allocation)."""
     import torch
@@ -388,19 +391,22 @@ def fc_attn_bwd_noalloc(view: View, q, k_loc, v_loc, k_recv, v_recv, o, lse, dou
         view.handle, _ptr(q, (tq, hq, d), bf, "q"), _ptr(k_loc, (tq, hkv, d), bf, "k_loc"),
         _ptr(v_loc, (tq, hkv, d), bf, "v_loc"), _ptr(k_recv, (tr, hkv, d), bf, "k_recv"),
         _ptr(v_recv, (tr, hkv, d), bf, "v_recv"), _ptr(o, (tq, hq, d), bf, "o"),
-        _ptr(lse, (hq, tq), f32, "lse"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
+        _ptr(o_f32, (tq, hq, d), f32, "o_f32"), _ptr(lse, (hq, tq), f32, "lse"), _ptr(dout, (tq, hq, d), bf, "dout"), float(scale),
         int(bool(deterministic)),
         _ptr(dq, (tq, hq, d), f32, "dq"), _ptr(dk_loc, (tq, hkv, d), f32, "dk_loc"),
         _ptr(dv_loc, (tq, hkv, d), f32, "dv_loc"), _ptr(dk_recv, (tr, hkv, d), f32, "dk_recv"),
         _ptr(dv_recv, (tr, hkv, d), f32, "dv_recv"), _stream()))
 
 
-def fc_bwd_preprocess(view: View, o, dout, delta):
+def fc_bwd_preprocess(view: View, o, dout, delta, o_f32=None):
+    """delta from the bf16 o, or from o_f32 when given (o may then be None)."""
     import torch
     i = view.info
     tq, hq, d = i["t_q"], i["hq"], i["d"]
     _check(lib().fc_bwd_preprocess(
-        view.handle, _ptr(o, (tq, hq, d), torch.bfloat16, "o"), _ptr(dout, (tq, hq, d), torch.bfloat16, "dout"),
+        view.handle, _ptr(o, (tq, hq, d), torch.bfloat16, "o"),
+        _ptr(o_f32, (tq, hq, d), torch.float32, "o_f32"),
+        _ptr(dout, (tq, hq, d), torch.bfloat16, "dout"),
         _ptr(delta, (hq, tq), torch.float32, "delta"), _stream()))
 
 

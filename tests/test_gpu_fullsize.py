@@ -1,17 +1,28 @@
-"""GPU parity at the workloads' full sizes, in the launch configuration the
-benchmark times (gather; both forward partial passes in one launch; LSE
-merge; preprocess; dK/dV and dQ workgroups in one launch), against the fp64
-oracle on outputs it can compute one by one:
+"""GPU parity at the workloads' full sizes, in the launch sequence bench.py
+times -- fc_kv_gather; fc_attn_fwd (FC_TWO_PASS: both partial passes and
+their LSE merge in one launch); fc_bwd_preprocess; fc_attn_bwd_pass
+(deterministic) -- against the oracle on the same bf16 inputs. The oracle
+runs in fp32 here (its fp64 form is what the CPU tests pin; the two differ
+by ~1e-6, far below the bounds) so that whole rank shares fit in seconds.
 
-* O, LSE and dQ on sampled query rows (every head), including the first and
-  last rows of pieces;
-* dK and dV on every key of a few whole documents (the oracle backward
-  restricted to a document's queries is exact for that document's keys);
-* the gathered K/V bit-exact; every output finite.
+Coverage, per workload and tensor seed (the length seed is the workload's
+own; tensor seeds 0, 1, 2 offset the workload's tensor seed):
+* every row of O, LSE and dQ and every key of dK and dV, local and received,
+  of every document segment of the rank;
+* except the one huge segment of the long-document and hybrid workloads (a
+  96K- / 131K-token document of which the rank holds 6144 / 2972 queries
+  that see 46080 / 83245 received keys): with the first seed, every row and
+  key of KV head 0 and its query heads; with the others it is skipped;
+* the merged forward bit-equal to the partial passes followed by
+  fc_lse_merge; the gathered K/V bit-exact; the product planner equal to the
+  oracle planner.
 
-Tolerances as in test_gpu_parity.py.
+Tolerances: O, dQ, dK, dV max-abs <= 2e-2 (the bound), LSE |err| <= 1e-3
+relative (max(1, |LSE|) below 1); dK/dV also <= 1.5e-2, a margin below the
+bound, on every seed.
 """
 import sys
+import time
 
 import numpy as np
 import pytest
@@ -19,7 +30,6 @@ import torch
 
 import _cases
 from oracle import attention as A
-from oracle import planner as OP
 from paper_2606_08476_amd import flashcp as F
 from paper_2606_08476_amd import synth
 
@@ -27,6 +37,8 @@ pytestmark = pytest.mark.gpu
 
 TOL = 2e-2
 LSE_TOL = 1e-3
+DKDV_MARGIN = 1.5e-2
+HUGE = 2e7   # query rows x (local + received keys) above which a segment is "huge"
 
 
 def say(*a):
@@ -38,102 +50,131 @@ def dev():
     if not torch.cuda.is_available():
         pytest.fail("GPU tests need a GPU")
     F.lib()
+    torch.set_num_threads(16)
     return torch.device("cuda:0")
 
 
-def _sample_rows(view, rng, n=48):
-    rows = set()
-    for s, qs, qe, _, _ in view.pieces.tolist():
-        rows.update((qs, qe - 1))
-    rows = sorted(rows)
-    rng.shuffle(rows)
-    rows = rows[: n // 2]
-    rows += rng.choice(len(view.q_gpos), size=n - len(rows), replace=False).tolist()
-    return np.unique(np.asarray(rows, dtype=np.int64))
-
-
-def _check_segments(view, nmax=3):
-    """The cheapest document segments by oracle cost, a mid-sized one and the
-    largest one (when the oracle can afford it: on the Whole-Doc workload its
-    key tiles are the ones the backward splits across workgroups)."""
-    qcu, rcu = view.q_cu_docseg, view.recv_cu
-    cost = [(int(qcu[s + 1] - qcu[s]) * int(qcu[s + 1] - qcu[s] + rcu[s + 1] - rcu[s]), s)
-            for s in range(len(view.seg_doc))]
-    cost.sort()
-    pick = [s for _, s in cost[:nmax - 1]]
-    for c, s in (cost[len(cost) // 2], cost[-1]):   # a mid-sized and the largest document
-        if s not in pick and c < 4e7:
-            pick.append(s)
-    return pick
-
-
-@pytest.mark.parametrize("name", list(synth.WORKLOADS))
-def test_full_size(name, dev):
-    case = _cases.make_case(name, name)
-    w = synth.WORKLOADS[name]
-    # the product planner agrees with the oracle on the full workload
-    plan_c = {"per_doc": F.fc_plan_per_doc, "whole_lpt": F.fc_plan_whole_lpt}.get(
-        w.plan, lambda cu, n: F.fc_plan_hybrid(cu, n)[0])(case.cu, case.cp)
-    assert np.array_equal(plan_c, case.plan)
-    say(f"[gpu-full] {name}: rank {case.rank}, t_q {case.oview.q_gpos.size}, t_recv {case.oview.recv_gpos.size}")
-    x = _cases.inputs(case)
-    xd = {k: v.to(dev) for k, v in x.items()}
-    v = F.View(case.cu, plan_c, case.cp, case.rank, case.hq, case.hkv, case.d).bind(dev)
+def bench_sequence(case, x, dev, o_f32=True):
+    """The bench's step on one case (by default, like the bench, the forward
+    also writes its fp32 O and delta is taken from it): returns the view and
+    every output (CPU copies), after checking the gather and the merged
+    forward's bits."""
+    v = F.View(case.cu, case.plan, case.cp, case.rank, case.hq, case.hkv, case.d).bind(dev)
     i = v.info
     tq, tr, hq, hkv, d = i["t_q"], i["t_recv"], case.hq, case.hkv, case.d
     bf, f32 = torch.bfloat16, torch.float32
     e = lambda *s, dt=f32: torch.empty(*s, dtype=dt, device=dev)
+    xd = {k: t.to(dev) for k, t in x.items()}
     kl, vl, kr, vr = e(tq, hkv, d, dt=bf), e(tq, hkv, d, dt=bf), e(tr, hkv, d, dt=bf), e(tr, hkv, d, dt=bf)
     F.fc_kv_gather(v, xd["k_pk"], xd["v_pk"], kl, vl, kr, vr)
-    oa, ob, la, lb = e(tq, hq, d), e(tq, hq, d), e(hq, tq), e(hq, tq)
     o, lse, delta = e(tq, hq, d, dt=bf), e(hq, tq), e(hq, tq)
-    if tr:
-        F.fc_attn_fwd_partials(v, xd["q"], kl, vl, kr, vr, 0.0, oa, la, ob, lb)
-        F.fc_lse_merge(oa, la, ob, lb, o, None, lse)
-    else:
-        ws = torch.empty(1, dtype=torch.uint8, device=dev)
-        F.fc_attn_fwd(v, xd["q"], kl, vl, kr, vr, 0.0, F.FC_TWO_PASS, o, None, lse, ws)
-    F.fc_bwd_preprocess(v, o, xd["do"], delta)
+    o32 = e(tq, hq, d) if o_f32 else None
+    fws = torch.empty(max(v.workspace_size(F.FC_TWO_PASS)[0], 1), dtype=torch.uint8, device=dev)
+    F.fc_attn_fwd(v, xd["q"], kl, vl, kr, vr, 0.0, F.FC_TWO_PASS, o, o32, lse, fws)
+    F.fc_bwd_preprocess(v, o, xd["do"], delta, o_f32=o32)
     dq, dkl, dvl, dkr, dvr = e(tq, hq, d), e(tq, hkv, d), e(tq, hkv, d), e(tr, hkv, d), e(tr, hkv, d)
     ws = torch.empty(max(v.workspace_size()[2], 1), dtype=torch.uint8, device=dev)
     F.fc_attn_bwd_pass(v, xd["q"], kl, vl, kr, vr, lse, delta, xd["do"], 0.0, dq, dkl, dvl, dkr, dvr, ws)
-    # the separate dK/dV and dQ kernels give the same bits
-    dq2, dkl2, dvl2, dkr2, dvr2 = (torch.empty_like(t) for t in (dq, dkl, dvl, dkr, dvr))
-    F.fc_attn_bwd_dkdv(v, xd["q"], kl, vl, kr, vr, lse, delta, xd["do"], 0.0, dkl2, dvl2, dkr2, dvr2, ws)
-    F.fc_attn_bwd_dq(v, xd["q"], kl, vl, kr, vr, lse, delta, xd["do"], 0.0, dq2)
+    # the merged forward writes exactly what the partial passes + merge write
+    if tr:
+        oa, ob, la, lb = e(tq, hq, d), e(tq, hq, d), e(hq, tq), e(hq, tq)
+        F.fc_attn_fwd_partials(v, xd["q"], kl, vl, kr, vr, 0.0, oa, la, ob, lb)
+        o2, l2 = e(tq, hq, d, dt=bf), e(hq, tq)
+        F.fc_lse_merge(oa, la, ob, lb, o2, None, l2)
     torch.cuda.synchronize()
-    say(f"[gpu-full] {name}: GPU done")
-    for a, b in ((dq, dq2), (dkl, dkl2), (dvl, dvl2), (dkr, dkr2), (dvr, dvr2)):
-        assert torch.equal(a, b)
-
+    if tr:
+        assert torch.equal(o, o2) and torch.equal(lse, l2)
     assert torch.equal(kl.cpu(), x["k_loc"]) and torch.equal(vl.cpu(), x["v_loc"])
     assert torch.equal(kr.cpu(), x["k_recv"]) and torch.equal(vr.cpu(), x["v_recv"])
-    for t in (o, lse, dq, dkl, dvl, dkr, dvr):
-        assert torch.isfinite(t).all()
+    out = {n: t.cpu() for n, t in dict(o=o, lse=lse, dq=dq, dk_loc=dkl, dv_loc=dvl,
+                                        dk_recv=dkr, dv_recv=dvr).items()}
+    for n, t in out.items():
+        assert torch.isfinite(t).all(), n
+    return v, out
 
+
+def compare(case, x, out, huge_group):
+    """Max errors of the GPU outputs against the oracle over the coverage in
+    the module docstring (huge_group: check the huge segment for KV head 0,
+    else skip it)."""
     ov = case.oview
     kv = np.concatenate([ov.q_gpos, ov.recv_gpos])
     K = torch.cat([x["k_loc"], x["k_recv"]])
     V = torch.cat([x["v_loc"], x["v_recv"]])
-    rng = np.random.default_rng(0)
-    rows = _sample_rows(ov, rng)
-    O_ref, L_ref = A.attention_fwd(case.cu, ov.q_gpos, x["q"], kv, K, V, rows=rows)
-    dq_ref, _, _ = A.attention_bwd(case.cu, ov.q_gpos, x["q"], kv, K, V, x["do"], rows=rows)
-    eo = float((o.cpu()[rows].double() - O_ref[rows]).abs().max())
-    el = float(((lse.cpu()[:, rows].double() - L_ref[:, rows]).abs() / L_ref[:, rows].abs().clamp_min(1)).max())
-    eq = float((dq.cpu()[rows].double() - dq_ref[rows]).abs().max())
-    say(f"[gpu-full] {name}: {rows.size} rows: O {eo:.3e} LSE {el:.3e} dQ {eq:.3e}")
-    assert eo <= TOL and el <= LSE_TOL and eq <= TOL
+    tq = ov.q_gpos.size
+    qcu, rcu = ov.q_cu_docseg, ov.recv_cu
+    nseg = len(ov.seg_doc)
+    cost = [int(qcu[s + 1] - qcu[s]) * int(qcu[s + 1] - qcu[s] + rcu[s + 1] - rcu[s]) for s in range(nseg)]
+    huge = [s for s in range(nseg) if cost[s] > HUGE]
+    G = case.hq // case.hkv
+    err = dict(o=0.0, lse=0.0, dq=0.0, dk=0.0, dv=0.0)
 
-    for s in _check_segments(ov):
-        q0, q1 = int(ov.q_cu_docseg[s]), int(ov.q_cu_docseg[s + 1])
-        r0, r1 = int(ov.recv_cu[s]), int(ov.recv_cu[s + 1])
-        seg_rows = np.arange(q0, q1)
-        _, dk_ref, dv_ref = A.attention_bwd(case.cu, ov.q_gpos, x["q"], kv, K, V, x["do"], rows=seg_rows)
-        ek = max(float((dkl.cpu()[q0:q1].double() - dk_ref[q0:q1]).abs().max()),
-                 float((dkr.cpu()[r0:r1].double() - dk_ref[tq + r0:tq + r1]).abs().max()) if r1 > r0 else 0.0)
-        ev = max(float((dvl.cpu()[q0:q1].double() - dv_ref[q0:q1]).abs().max()),
-                 float((dvr.cpu()[r0:r1].double() - dv_ref[tq + r0:tq + r1]).abs().max()) if r1 > r0 else 0.0)
-        say(f"[gpu-full] {name}: segment {s} ({q1 - q0} local, {r1 - r0} received keys): dK {ek:.3e} dV {ev:.3e}")
-        assert ek <= TOL and ev <= TOL
+    def acc(rows, keys_l, keys_r, heads, kvh, res):
+        dq_r, dk_r, dv_r, O_r, L_r = res
+        hs = torch.as_tensor(heads)
+        rr = torch.as_tensor(rows)
+        err["o"] = max(err["o"], float((out["o"][rr][:, hs].double() - O_r[rr][:, hs].double()).abs().max()))
+        lr = L_r[hs][:, rr].double()
+        err["lse"] = max(err["lse"], float(((out["lse"][hs][:, rr].double() - lr).abs() / lr.abs().clamp_min(1)).max()))
+        err["dq"] = max(err["dq"], float((out["dq"][rr][:, hs].double() - dq_r[rr][:, hs].double()).abs().max()))
+        jj = torch.as_tensor(kvh)
+        for name, ref in (("dk", dk_r), ("dv", dv_r)):
+            ref = ref[:, jj].double()
+            parts = []
+            if keys_l.size:
+                parts.append((out[name + "_loc"][torch.as_tensor(keys_l)][:, jj].double() - ref[torch.as_tensor(keys_l)]).abs().max())
+            if keys_r.size:
+                parts.append((out[name + "_recv"][torch.as_tensor(keys_r)][:, jj].double() - ref[tq + torch.as_tensor(keys_r)]).abs().max())
+            if parts:
+                err[name] = max(err[name], float(max(parts)))
+
+    rest = [s for s in range(nseg) if s not in huge]
+    if rest:
+        rows = np.concatenate([np.arange(qcu[s], qcu[s + 1]) for s in rest])
+        kl = rows
+        kr = np.concatenate([np.arange(rcu[s], rcu[s + 1]) for s in rest]).astype(np.int64)
+        t0 = time.time()
+        res = A.attention_bwd(case.cu, ov.q_gpos, x["q"], kv, K, V, x["do"], rows=rows,
+                              dtype=torch.float32, with_fwd=True)
+        acc(rows, kl, kr, list(range(case.hq)), list(range(case.hkv)), res)
+        say(f"[gpu-full] {case.name}: {len(rest)} segments, {rows.size} rows, all heads: oracle {time.time() - t0:.1f} s")
+    if huge_group:
+        for s in huge:
+            rows = np.arange(qcu[s], qcu[s + 1])
+            kr = np.arange(rcu[s], rcu[s + 1])
+            t0 = time.time()
+            res = A.attention_bwd(case.cu, ov.q_gpos, x["q"], kv, K, V, x["do"], rows=rows,
+                                  dtype=torch.float32, kv_heads=[0], with_fwd=True)
+            acc(rows, rows, kr, list(range(G)), [0], res)
+            say(f"[gpu-full] {case.name}: huge segment {s} ({rows.size} rows, {kr.size} received keys), "
+                f"KV head 0: oracle {time.time() - t0:.1f} s")
+    return err, huge
+
+
+def seeded_case(name, seed):
+    case = _cases.make_case(name, name)
+    if seed:
+        case.seed = case.seed + 1000 * seed
+    return case
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("name", list(synth.WORKLOADS))
+def test_full_size(name, seed, dev):
+    case = seeded_case(name, seed)
+    w = synth.WORKLOADS[name]
+    if seed == 0:
+        plan_c = {"per_doc": F.fc_plan_per_doc, "whole_lpt": F.fc_plan_whole_lpt}.get(
+            w.plan, lambda cu, n: F.fc_plan_hybrid(cu, n)[0])(case.cu, case.cp)
+        assert np.array_equal(plan_c, case.plan)
+    say(f"[gpu-full] {name} seed {seed}: rank {case.rank}, t_q {case.oview.q_gpos.size}, "
+        f"t_recv {case.oview.recv_gpos.size}, tensor seed {case.seed}")
+    x = _cases.inputs(case)
+    v, out = bench_sequence(case, x, dev)
     v.close()
+    say(f"[gpu-full] {name} seed {seed}: GPU done")
+    err, huge = compare(case, x, out, huge_group=seed == 0)
+    say(f"[gpu-full] {name} seed {seed}: " + " ".join(f"{k} {e:.3e}" for k, e in err.items()) +
+        (f" (huge segments {huge} {'KV head 0' if seed == 0 else 'skipped'})" if huge else ""))
+    assert err["o"] <= TOL and err["dq"] <= TOL and err["lse"] <= LSE_TOL
+    assert err["dk"] <= DKDV_MARGIN and err["dv"] <= DKDV_MARGIN

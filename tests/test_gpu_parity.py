@@ -82,9 +82,10 @@ class Run:
         self.dk_recv = torch.empty(tr, hkv, d, dtype=f32, device=dev)
         self.dv_recv = torch.empty_like(self.dk_recv)
         bws_t = torch.empty(bws, dtype=torch.uint8, device=dev)
+        # delta from the fp32 O, as the benchmark's step computes it
         F.fc_attn_bwd(self.v, self.q, self.k_loc, self.v_loc, self.k_recv, self.v_recv, self.o,
                       self.lse, self.do, 0.0, self.dq, self.dk_loc, self.dv_loc, self.dk_recv,
-                      self.dv_recv, bws_t)
+                      self.dv_recv, bws_t, o_f32=self.o32)
         torch.cuda.synchronize()
         say(f"[gpu] case={case.name} done")
 
@@ -284,9 +285,9 @@ def test_backward_atomic(key, dev):
     ws = torch.empty(bws, dtype=torch.uint8, device=dev)
     a = r.bwd_outputs()
     F.fc_attn_bwd(r.v, r.q, r.k_loc, r.v_loc, r.k_recv, r.v_recv, r.o, r.lse, r.do, 0.0, *a, ws,
-                  deterministic=False)
+                  deterministic=False, o_f32=r.o32)
     delta = torch.empty_like(r.lse)
-    F.fc_bwd_preprocess(r.v, r.o, r.do, delta)
+    F.fc_bwd_preprocess(r.v, None, r.do, delta, o_f32=r.o32)
     b = r.bwd_outputs()
     pws_t = torch.empty(max(pws, 1), dtype=torch.uint8, device=dev)
     F.fc_attn_bwd_pass(r.v, r.q, r.k_loc, r.v_loc, r.k_recv, r.v_recv, r.lse, delta, r.do, 0.0,
@@ -302,6 +303,24 @@ def test_backward_atomic(key, dev):
     e_ref = max(_maxabs(a[0], dq_ref), _maxabs(b[0], dq_ref))
     say(f"[gpu] {key} bwd atomic: dQ vs oracle {e_ref:.3e}, vs deterministic {e_order:.3e}")
     assert e_ref <= G_TOL and e_order <= DQ_ORDER_TOL
+
+
+@pytest.mark.parametrize("key", ["tiny", "llama8b_8k", "short_docs"])
+def test_backward_delta_from_bf16_output(key, dev):
+    """The backward given only the bf16 O (delta from it): within the bound
+    of the oracle, and each gradient within 2e-2 of the fp32-O run."""
+    r = get_run(key, dev)
+    _, bws, _ = r.v.workspace_size()
+    ws = torch.empty(bws, dtype=torch.uint8, device=dev)
+    a = r.bwd_outputs()
+    F.fc_attn_bwd(r.v, r.q, r.k_loc, r.v_loc, r.k_recv, r.v_recv, r.o, r.lse, r.do, 0.0, *a, ws)
+    torch.cuda.synchronize()
+    dq, dk, dv = r.oracle_bwd()
+    tq = r.v.info["t_q"]
+    e = dict(dq=_maxabs(a[0], dq), dk_loc=_maxabs(a[1], dk[:tq]), dv_loc=_maxabs(a[2], dv[:tq]),
+             dk_recv=_maxabs(a[3], dk[tq:]), dv_recv=_maxabs(a[4], dv[tq:]))
+    say(f"[gpu] {key} bwd (delta from bf16 O): " + " ".join(f"{k} {v:.3e}" for k, v in e.items()))
+    assert max(e.values()) <= G_TOL, e
 
 
 def test_document_isolation_on_gpu(dev):

@@ -173,9 +173,10 @@ def test_kernel_calls_rejected_before_launch():
     assert lib.fc_kv_gather(h, 1, 1, 128, 1, 1, 1, 1, None) == -5
     assert lib.fc_attn_fwd(h, 1, 1, 1, 1, 1, 0.0, 0, 1, None, 1, None, 0, None) == -5
     for det in (0, 1):
-        assert lib.fc_attn_bwd(h, *([1] * 8), 0.0, det, *([1] * 5), None, 0, None) == -5
+        assert lib.fc_attn_bwd(h, *([1] * 9), 0.0, det, *([1] * 5), None, 0, None) == -5
         assert lib.fc_attn_bwd_pass(h, *([1] * 8), 0.0, det, *([1] * 5), None, 0, None) == -5
-        assert lib.fc_attn_bwd_noalloc(h, *([1] * 8), 0.0, det, *([1] * 5), None) == -5
+        assert lib.fc_attn_bwd_noalloc(h, *([1] * 9), 0.0, det, *([1] * 5), None) == -5
+    assert lib.fc_bwd_preprocess(h, 1, None, 1, 1, None) == -5
     assert lib.fc_attn_bwd_dkdv(h, *([1] * 8), 0.0, *([1] * 4), None, 0, None) == -5
     assert lib.fc_attn_fwd_partial(h, 0, 1, 1, 1, 0.0, 1, 1, None) == -5
     assert lib.fc_attn_fwd_partials(h, 1, 1, 1, 1, 1, 0.0, 1, 1, 1, 1, None) == -5

@@ -217,3 +217,29 @@ def test_row_restricted_backward_is_exact_for_its_documents():
     assert torch.allclose(dv2[rows], dv[rows], atol=1e-14)
     other = np.setdiff1d(ar, rows)
     assert torch.all(dq2[other] == 0) and torch.all(dk2[other] == 0)
+
+
+def test_kv_head_restriction_equals_unrestricted():
+    """Restricting the oracle to some KV heads computes exactly the values of
+    the unrestricted call for those heads' query heads and KV rows (each head
+    is computed on its own), and NaN elsewhere; with_fwd returns the
+    forward's O and LSE alongside."""
+    lens = [23, 40, 9]
+    cu, q, k, v, do = _packed(lens, 8, 4, 8, 13)
+    T = cu[-1]
+    ar = np.arange(T)
+    O, L = A.attention_fwd(cu, ar, q, ar, k, v, 0.3)
+    dq, dk, dv = A.attention_bwd(cu, ar, q, ar, k, v, do, 0.3)
+    for sel in ([1], [0, 3]):
+        hs = [h for h in range(8) if h // 2 in sel]
+        oth = [h for h in range(8) if h not in hs]
+        kvo = [j for j in range(4) if j not in sel]
+        O2, L2 = A.attention_fwd(cu, ar, q, ar, k, v, 0.3, kv_heads=sel)
+        assert torch.equal(O2[:, hs], O[:, hs]) and torch.equal(L2[hs], L[hs])
+        assert torch.isnan(O2[:, oth]).all() and torch.isnan(L2[oth]).all()
+        dq2, dk2, dv2, O3, L3 = A.attention_bwd(cu, ar, q, ar, k, v, do, 0.3, kv_heads=sel,
+                                                with_fwd=True)
+        assert torch.equal(dq2[:, hs], dq[:, hs]) and torch.isnan(dq2[:, oth]).all()
+        assert torch.equal(dk2[:, sel], dk[:, sel]) and torch.equal(dv2[:, sel], dv[:, sel])
+        assert torch.isnan(dk2[:, kvo]).all() and torch.isnan(dv2[:, kvo]).all()
+        assert torch.equal(O3[:, hs], O[:, hs]) and torch.equal(L3[hs], L[hs])
