@@ -43,11 +43,18 @@ def parse():
     ap.add_argument("--delta-from", choices=["f32", "bf16"], default="f32",
                     help="output the backward preprocess reads: the forward's fp32 O (also "
                          "written by the forward) or its bf16 O")
+    ap.add_argument("--bm-fwd", type=int, default=0,
+                    help="forward / dQ query tile rows (32, 64, 128; 0: the view's default)")
+    ap.add_argument("--workloads", type=int, default=1,
+                    help="also time the other workloads (GPU legs only) into the 'workloads' key")
+    ap.add_argument("--workload-steps", type=int, default=10,
+                    help="timed steps of each other workload")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU-oracle baseline sample (0 disables it)")
-    ap.add_argument("--study", choices=["planner", "granularity"], default=None,
+    ap.add_argument("--study", choices=["planner", "granularity", "tiles"], default=None,
                     help="instead of the step benchmark: the planner-quality study (host "
-                         "only) or the shard-granularity kernel study; JSON lines, then a table")
+                         "only), the shard-granularity kernel study, or the forward tile-shape "
+                         "sweep; JSON lines, then a table")
     ap.add_argument("--seeds", type=int, default=5, help="length seeds per planner-study row")
     return ap.parse_args()
 
@@ -318,29 +325,21 @@ def study_granularity(args):
               f"{r['max_rank_ms']} | {r['tflops_sum']} | {r['tflops_n_x_max']} |")
 
 
-def main():
-    args = parse()
-    if args.study == "planner":
-        study_planner(args)
-        return
-    if args.study == "granularity":
-        study_granularity(args)
-        return
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs one rank's share on one GPU; --gpus must be 1 "
-              "(multi-GPU exchange is not part of it)", file=sys.stderr)
-        sys.exit(2)
+def measure(args, name, steps, warmup, dev):
+    """The timed step on one workload: plan, view, gather, two-pass forward,
+    preprocess, backward pass; per-kernel times from HIP events on the
+    step's stream, the step from the host clock around `steps` steps."""
     import torch
     from paper_2606_08476_amd import flashcp as F
     from paper_2606_08476_amd import synth
 
-    w = synth.WORKLOADS[args.workload]
-    lens = synth.doc_lengths(args.workload)
+    w = synth.WORKLOADS[name]
+    lens = synth.doc_lengths(name)
     cu = synth.cu_seqlens(lens)
-    dev = torch.device("cuda:0")
     plan = plan_for(F, w, cu)
     rank = rank_for(F, w, cu, plan)
-    view = F.View(cu, plan, w.cp, rank, w.hq, w.hkv, w.d)
+    tiles = (args.bm_fwd, 0, 0, 0)
+    view = F.View(cu, plan, w.cp, rank, w.hq, w.hkv, w.d, tiles=tiles)
     info = view.info
     tab = view.export()
     tq, tr, hq, hkv, d = info["t_q"], info["t_recv"], w.hq, w.hkv, w.d
@@ -384,9 +383,9 @@ def main():
     acc = np.zeros(len(names))
     kept = []
 
-    def step(timed):
+    def step():
         p = plan_for(F, w, cu)
-        v = F.View(cu, p, w.cp, rank, hq, hkv, d).bind(dev, meta)
+        v = F.View(cu, p, w.cp, rank, hq, hkv, d, tiles=tiles).bind(dev, meta)
         kept.append(v)
         ev[0].record()
         F.fc_kv_gather(v, k_pk, v_pk, k_loc, v_loc, k_recv, v_recv)
@@ -405,14 +404,14 @@ def main():
                            dv_loc, dk_recv, dv_recv, dkdv_ws, deterministic=args.bwd == "det")
         ev[4].record()
 
-    for _ in range(args.warmup):
-        step(False)
+    for _ in range(warmup):
+        step()
     torch.cuda.synchronize()
     kept.clear()
     t0 = time.perf_counter()
     per = []
-    for _ in range(args.steps):
-        step(True)
+    for _ in range(steps):
+        step()
         # per-kernel durations are read after the loop from stored copies
         per.append([ev[i] for i in range(len(ev))])
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
@@ -421,7 +420,7 @@ def main():
     for e in per:
         for i in range(len(names)):
             acc[i] += e[i].elapsed_time(e[i + 1])
-    acc /= args.steps
+    acc /= steps
     # the merge kernel alone (outside the timed steps): the step merges in the
     # forward's epilogue, this is fc_lse_merge for partials made apart
     merge_side = None
@@ -447,8 +446,9 @@ def main():
     for v in kept:
         v.close()
     kept.clear()
+    view.close()
 
-    ms = wall * 1e3 / args.steps
+    ms = wall * 1e3 / steps
     useful = 14.0 * d * hq * pairs
     value = useful / (ms * 1e-3) / 1e12
     # per-kernel algorithmic work
@@ -460,11 +460,12 @@ def main():
         # dO (bf16) and O (fp32, or bf16) read, delta written
         "bwd_preprocess": ("hbm", tq * hq * (2 * d + (4 if o32 is not None else 2) * d + 4)),
         # backward, algorithmic: S recomputed once, dP, dV, dK, dQ (10d per
-        # pair, the FlashAttention count); the kernels execute 14d (the dQ
-        # workgroups recompute S and dP), reported apart as executed_tflops
+        # pair, the FlashAttention count); the deterministic kernels execute
+        # 14d (the dQ workgroups recompute S and dP), reported apart as
+        # executed_tflops
         "attn_bwd": ("mfma", 10.0 * d * hq * pairs),
     }
-    executed = {"attn_bwd": 14.0 * d * hq * pairs}
+    executed = {"attn_bwd": (14.0 if args.bwd == "det" else 10.0) * d * hq * pairs}
     kernels = {}
     for i, n in enumerate(names):
         kind, amount = work[n]
@@ -492,26 +493,109 @@ def main():
         ach = amount / (acc[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": dn}
+    return dict(w=w, rank=rank, cu=cu, tab=tab, x=x, tq=tq, tr=tr, pairs=pairs, useful=useful,
+                bm_fwd=info["bm_fwd"],
+                ms=ms, value=value, kernels=kernels, roof=roof, merge_side=merge_side,
+                steps=steps, warmup=warmup)
 
+
+def study_tiles(args):
+    """Forward / dQ query-tile shape against step time on every workload:
+    bm_fwd = 32, 64, 128 rows (4, 2, 1 query heads of a KV group per
+    workgroup; the shapes the group size allows), the step timed as in the
+    benchmark."""
+    import torch
+    from paper_2606_08476_amd import synth
+    dev = torch.device("cuda:0")
+    rows = []
+    for name, w in synth.WORKLOADS.items():
+        G = w.hq // w.hkv
+        for bm in (32, 64, 128):
+            if G % (128 // bm):
+                continue
+            args.bm_fwd = bm
+            m = measure(args, name, args.workload_steps, 2, dev)
+            k = m["kernels"]
+            row = {"study": "tiles", "workload": name, "bm_fwd": bm, "ms_per_step": round(m["ms"], 4),
+                   "tflops": round(m["value"], 1), "fwd_ms": k["attn_fwd"]["ms"],
+                   "bwd_ms": k["attn_bwd"]["ms"]}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+            del m
+            torch.cuda.empty_cache()
+    print("\n| workload | bm_fwd | step ms | TFLOP/s | forward ms | backward ms |")
+    print("|---|---|---|---|---|---|")
+    for r in rows:
+        print(f"| {r['workload']} | {r['bm_fwd']} | {r['ms_per_step']} | {r['tflops']} | "
+              f"{r['fwd_ms']} | {r['bwd_ms']} |")
+
+
+def describe(m):
+    w = m["w"]
+    return (f"{w.name}: {w.context}-token packed context, CP degree {w.cp}, {w.plan} plan, "
+            f"rank {m['rank']}; {w.hq} query / {w.hkv} KV heads, d {w.d}")
+
+
+def main():
+    args = parse()
+    if args.study == "planner":
+        study_planner(args)
+        return
+    if args.study == "granularity":
+        study_granularity(args)
+        return
+    if args.study == "tiles":
+        study_tiles(args)
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs one rank's share on one GPU; --gpus must be 1 "
+              "(multi-GPU exchange is not part of it)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_08476_amd import synth
+
+    dev = torch.device("cuda:0")
+    m = measure(args, args.workload, args.steps, args.warmup, dev)
+    w, d, hq = m["w"], m["w"].d, m["w"].hq
+    ms, value = m["ms"], m["value"]
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: {w.context}-token packed context, CP degree {w.cp}, "
-                               f"{w.plan} plan, rank {rank}; {hq} query / {hkv} KV heads, d {d}; "
-                               "two-pass forward (received and local partials and their LSE merge in one launch), "
-                               "key-major dK/dV and query-major dQ backward",
-                   "t_q": tq, "t_recv": tr, "pairs_per_head": pairs,
-                   "useful_tflop_per_step": round(useful / 1e12, 4),
+        "config": {"workload": describe(m) + "; two-pass forward (received and local partials and "
+                               "their LSE merge in one launch), key-major dK/dV and query-major dQ "
+                               "backward" + ("" if args.bwd == "det" else " (dQ by atomics)"),
+                   "t_q": m["tq"], "t_recv": m["tr"], "pairs_per_head": m["pairs"],
+                   "useful_tflop_per_step": round(m["useful"] / 1e12, 4),
                    "pct_of_bf16_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
-                   "strict_tflops_12d": round(12.0 * d * hq * pairs / (ms * 1e-3) / 1e12, 2)},
-        "roofline": roof,
-        "kernels": kernels,
-        "lse_merge_alone": merge_side,
+                   "strict_tflops_12d": round(12.0 * d * hq * m["pairs"] / (ms * 1e-3) / 1e12, 2),
+                   "bwd_mode": "deterministic" if args.bwd == "det" else "atomic dQ",
+                   "bm_fwd": m["bm_fwd"],
+                   "delta_from": "fp32 O" if args.delta_from == "f32" else "bf16 O"},
+        "roofline": m["roof"],
+        "kernels": m["kernels"],
+        "lse_merge_alone": m["merge_side"],
     }
+    # the other workloads, GPU legs only, after the headline one
+    if args.workloads:
+        wl = {}
+        for name in synth.WORKLOADS:
+            r = m if name == args.workload else measure(args, name, args.workload_steps, 2, dev)
+            wl[name] = {
+                "config": describe(r), "t_q": r["tq"], "t_recv": r["tr"], "pairs_per_head": r["pairs"],
+                "bm_fwd": r["bm_fwd"],
+                "steps": r["steps"], "ms_per_step": round(r["ms"], 4), "tflops": round(r["value"], 2),
+                "pct_of_bf16_peak": round(100 * r["value"] / BF16_PEAK_TFLOPS, 2),
+                "kernels": r["kernels"], "roofline_kernel": r["roof"]["kernel"],
+                "roofline_frac": r["roof"]["frac"],
+                "lse_merge_alone_gbs": r["merge_side"]["gbs"] if r["merge_side"] else None}
+            if r is not m:
+                del r
+                torch.cuda.empty_cache()
+        out["workloads"] = wl
     if args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(cu, tab, x, w, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(m["cu"], m["tab"], m["x"], w, args.cpu_seconds)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

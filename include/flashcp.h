@@ -156,11 +156,26 @@ typedef struct {
   int64_t n_bwd_slots;
 } fc_view_info;
 
+/* Tile shapes of a view; 0 in a field selects its default.
+ *   bm_fwd  query rows per workgroup of the forward and of the dQ pass: 32,
+ *           64 or 128, i.e. 4, 2 or 1 query heads of a KV-head group per
+ *           workgroup (each wave takes 32 rows of one head); 128/bm_fwd must
+ *           divide Hq/Hkv. Default: as many heads per workgroup as the group
+ *           allows, min(Hq/Hkv, 4) (bm_fwd = 32 when Hq/Hkv >= 4).
+ *   bn_fwd  keys per forward / dQ tile: 64 (the compiled shape).
+ *   bm_bwd  query rows per dK/dV iteration: 32 (compiled).
+ *   bn_bwd  keys per dK/dV workgroup: 128 (compiled).
+ * Other values give FC_ERR_UNSUPPORTED. */
+typedef struct {
+  int32_t bm_fwd, bn_fwd, bm_bwd, bn_bwd;
+} fc_tile_cfg;
+
 /* Build rank `rank`'s view of a validated plan (FC_ERR_PLAN otherwise) for
- * hq query heads, hkv KV heads and head dim d. *out receives the view. */
+ * hq query heads, hkv KV heads and head dim d, with the tile shapes of
+ * `tiles` (NULL: all defaults). *out receives the view. */
 int fc_view_create(const int32_t* cu_seqlens, int32_t n_docs, const fc_shard* shards,
                    int64_t n_shards, int32_t cp, int32_t rank, int32_t hq, int32_t hkv,
-                   int32_t d, fc_view* out);
+                   int32_t d, const fc_tile_cfg* tiles, fc_view* out);
 
 int fc_view_get_info(fc_view view, fc_view_info* out);
 

@@ -219,7 +219,8 @@ void View::build_meta() {
 }
 
 int build_view(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_t n_shards,
-               int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d, View& v) {
+               int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d,
+               const fc_tile_cfg* tiles, View& v) {
   std::vector<int64_t> lens;
   if (int rc = doc_lengths(cu, n_docs, lens)) return rc;
   if (int rc = validate_plan(lens, cp, shards, n_shards, false)) return rc;
@@ -235,7 +236,23 @@ int build_view(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_
   v.hq = hq;
   v.hkv = hkv;
   v.d = d;
-  v.heads_per_tile = std::min(G, 4);
+  // tile shapes: the forward / dQ query tile is 32 rows per wave times the
+  // waves per head, 4 / (heads per workgroup); the other shapes are compiled
+  const fc_tile_cfg t = tiles ? *tiles : fc_tile_cfg{0, 0, 0, 0};
+  if (t.bm_fwd == 0) {
+    v.heads_per_tile = std::min(G, 4);
+  } else {
+    if (t.bm_fwd != 32 && t.bm_fwd != 64 && t.bm_fwd != 128)
+      return fail(FC_ERR_UNSUPPORTED, "bm_fwd must be 32, 64 or 128");
+    v.heads_per_tile = 128 / t.bm_fwd;
+    if (G % v.heads_per_tile)
+      return fail(FC_ERR_UNSUPPORTED, "bm_fwd " + std::to_string(t.bm_fwd) + " puts " +
+                                          std::to_string(v.heads_per_tile) +
+                                          " query heads in a workgroup; hq/hkv is " +
+                                          std::to_string(G));
+  }
+  if ((t.bn_fwd && t.bn_fwd != 64) || (t.bm_bwd && t.bm_bwd != 32) || (t.bn_bwd && t.bn_bwd != 128))
+    return fail(FC_ERR_UNSUPPORTED, "compiled tile shapes: bn_fwd 64, bm_bwd 32, bn_bwd 128");
   v.bm_fwd = 32 * (4 / v.heads_per_tile);
   v.bn_fwd = 64;
   v.bm_bwd = 32;
@@ -290,12 +307,13 @@ using namespace fc;
 extern "C" {
 
 int fc_view_create(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_t n_shards,
-                   int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d, fc_view* out) {
+                   int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d,
+                   const fc_tile_cfg* tiles, fc_view* out) {
   clear_error();
   if (!out) return fail(FC_ERR_INVALID_ARG, "out is null");
   *out = nullptr;
   View* v = new View();
-  if (int rc = build_view(cu, n_docs, shards, n_shards, cp, rank, hq, hkv, d, *v)) {
+  if (int rc = build_view(cu, n_docs, shards, n_shards, cp, rank, hq, hkv, d, tiles, *v)) {
     delete v;
     return rc;
   }

@@ -50,6 +50,7 @@ struct View {
 };
 
 int build_view(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_t n_shards,
-               int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d, View& v);
+               int32_t cp, int32_t rank, int32_t hq, int32_t hkv, int32_t d,
+               const fc_tile_cfg* tiles, View& v);
 
 }  // namespace fc

@@ -47,6 +47,11 @@ class Shard(C.Structure):
     _fields_ = [("doc", C.c_int32), ("rank", C.c_int32), ("offset", C.c_int32), ("len", C.c_int32)]
 
 
+class TileCfg(C.Structure):
+    _fields_ = [("bm_fwd", C.c_int32), ("bn_fwd", C.c_int32), ("bm_bwd", C.c_int32),
+                ("bn_bwd", C.c_int32)]
+
+
 class ViewInfo(C.Structure):
     _fields_ = [
         ("t_q", C.c_int32), ("t_recv", C.c_int32), ("n_seg", C.c_int32), ("n_pieces", C.c_int32),
@@ -86,7 +91,7 @@ def lib():
                               C.POINTER(C.c_int64), I32P, I32P, C.POINTER(C.c_int64), C.POINTER(C.c_int64),
                               C.POINTER(C.c_double)],
             "fc_view_create": [I32P, C.c_int32, C.POINTER(Shard), C.c_int64, C.c_int32, C.c_int32,
-                               C.c_int32, C.c_int32, C.c_int32, C.POINTER(P)],
+                               C.c_int32, C.c_int32, C.c_int32, C.POINTER(TileCfg), C.POINTER(P)],
             "fc_view_get_info": [P, C.POINTER(ViewInfo)],
             "fc_view_export": [P] + [I32P] * 11,
             "fc_view_bind": [P, P, C.c_size_t, P],
@@ -206,13 +211,16 @@ def fc_plan_stats(cu, cp: int, plan, hkv: int, d: int) -> dict:
 
 class View:
     """An fc_view handle plus, once bound, the device buffer holding its
-    tables. Destroyed with ``close()`` (or when garbage collected)."""
+    tables. Destroyed with ``close()`` (or when garbage collected).
+    ``tiles``: (bm_fwd, bn_fwd, bm_bwd, bn_bwd), 0 for a default; None for
+    all defaults."""
 
-    def __init__(self, cu, plan, cp: int, rank: int, hq: int, hkv: int, d: int):
+    def __init__(self, cu, plan, cp: int, rank: int, hq: int, hkv: int, d: int, tiles=None):
         a, p, n = _cu(cu)
         s, m = _shards(plan)
         h = P()
-        _check(lib().fc_view_create(p, n, s, m, cp, rank, hq, hkv, d, C.byref(h)))
+        t = C.byref(TileCfg(*[int(x) for x in tiles])) if tiles is not None else None
+        _check(lib().fc_view_create(p, n, s, m, cp, rank, hq, hkv, d, t, C.byref(h)))
         self._h = h
         self.meta = None
         info = ViewInfo()

@@ -25,10 +25,11 @@ class Case:
     d: int
     seed: int
     oview: OV.RankView
+    tiles: tuple | None = None
 
 
 def make_case(name, workload, context=None, cp=None, rank=None, hq=None, hkv=None, d=None,
-              seed=None, lens=None, plan=None) -> Case:
+              seed=None, lens=None, plan=None, tiles=None) -> Case:
     w = synth.WORKLOADS[workload]
     cp = w.cp if cp is None else cp
     if lens is None:
@@ -52,7 +53,7 @@ def make_case(name, workload, context=None, cp=None, rank=None, hq=None, hkv=Non
         else:
             rank = int(w.rank)
     return Case(name, cu, plan, cp, rank, hq or w.hq, hkv or w.hkv, d or w.d,
-                w.index if seed is None else seed, OV.rank_view(cu, plan, rank))
+                w.index if seed is None else seed, OV.rank_view(cu, plan, rank), tiles)
 
 
 def inputs(case: Case):
@@ -96,6 +97,9 @@ SMALL = {
     # 128-key tiles: no ragged tile anywhere, masks exactly on tile edges
     "aligned_docs": dict(workload="llama8b", cp=2, rank=0,
                          lens=[512, 1024, 256, 2048, 512]),
+    # forward / dQ query tiles of 64 and 128 rows (2 and 1 heads per workgroup)
+    "llama8b_8k_bm64": dict(workload="llama8b", context=8192, tiles=(64, 0, 0, 0)),
+    "longdoc_16k_bm128": dict(workload="longdoc", context=16384, tiles=(128, 0, 0, 0)),
 }
 
 

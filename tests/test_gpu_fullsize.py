@@ -59,7 +59,7 @@ def bench_sequence(case, x, dev, o_f32=True):
     also writes its fp32 O and delta is taken from it): returns the view and
     every output (CPU copies), after checking the gather and the merged
     forward's bits."""
-    v = F.View(case.cu, case.plan, case.cp, case.rank, case.hq, case.hkv, case.d).bind(dev)
+    v = F.View(case.cu, case.plan, case.cp, case.rank, case.hq, case.hkv, case.d, tiles=case.tiles).bind(dev)
     i = v.info
     tq, tr, hq, hkv, d = i["t_q"], i["t_recv"], case.hq, case.hkv, case.d
     bf, f32 = torch.bfloat16, torch.float32

@@ -58,7 +58,8 @@ class Run:
         say(f"[gpu] case={case.name} rank={case.rank} heads={case.hq}/{case.hkv} d={case.d} mode={mode}")
         self.x = _cases.inputs(case) if x is None else x
         x = {k: v.to(dev) for k, v in self.x.items()}
-        self.v = F.View(case.cu, case.plan, case.cp, case.rank, case.hq, case.hkv, case.d).bind(dev)
+        self.v = F.View(case.cu, case.plan, case.cp, case.rank, case.hq, case.hkv, case.d,
+                        tiles=case.tiles).bind(dev)
         i = self.v.info
         tq, tr, hq, hkv, d = i["t_q"], i["t_recv"], i["hq"], i["hkv"], i["d"]
         bf = torch.bfloat16

@@ -80,8 +80,8 @@ def test_planners_bit_exact_workloads(name):
         assert F.fc_plan_stats(cu, w.cp, plan, w.hkv, w.d) == P.stats(cu, w.cp, plan, w.hkv, w.d)
 
 
-def _compare_view(cu, plan, N, r, hq, hkv, d):
-    v = F.View(cu, plan, N, r, hq, hkv, d)
+def _compare_view(cu, plan, N, r, hq, hkv, d, tiles=None):
+    v = F.View(cu, plan, N, r, hq, hkv, d, tiles=tiles)
     e = v.export()
     o = V.rank_view(cu, plan, r)
     i = v.info
@@ -105,6 +105,37 @@ def test_views_bit_exact_random():
             for r in range(N):
                 for hq, hkv, d in ((4, 4, 64), (8, 2, 128), (16, 2, 128)):
                     _compare_view(cu, plan, N, r, hq, hkv, d)
+
+
+def test_tile_shapes():
+    """A view's forward query tile follows fc_tile_cfg.bm_fwd (32, 64 or 128
+    rows: 4, 2 or 1 heads of a KV group per workgroup) and its tile maps
+    equal the oracle's for that shape; shapes that are not compiled, or that
+    put more heads in a workgroup than the group has, are rejected."""
+    for cu, N in _random_cases(4, seed=21):
+        plan = P.plan_per_doc(cu, N)
+        for hq, hkv in ((16, 2), (8, 2), (4, 4)):
+            G = hq // hkv
+            for bm in (32, 64, 128):
+                if G % (128 // bm):
+                    with pytest.raises(F.FlashCPError) as ei:
+                        F.View(cu, plan, N, 0, hq, hkv, 64, tiles=(bm, 0, 0, 0))
+                    assert ei.value.code == -4
+                    continue
+                v = F.View(cu, plan, N, 0, hq, hkv, 64, tiles=(bm, 0, 0, 0))
+                assert v.info["bm_fwd"] == bm
+                v.close()
+                for r in range(N):
+                    _compare_view(cu, plan, N, r, hq, hkv, 64, tiles=(bm, 64, 32, 128))
+    cu, N = next(iter(_random_cases(1, seed=22)))
+    plan = P.plan_per_doc(cu, N)
+    # defaults: as many heads per workgroup as the group allows, up to 4
+    for hq, hkv, bm in ((32, 8, 32), (16, 8, 64), (8, 8, 128)):
+        assert F.View(cu, plan, N, 0, hq, hkv, 128).info["bm_fwd"] == bm
+    for bad in ((48, 0, 0, 0), (0, 128, 0, 0), (0, 0, 64, 0), (0, 0, 0, 64)):
+        with pytest.raises(F.FlashCPError) as ei:
+            F.View(cu, plan, N, 0, 32, 8, 128, tiles=bad)
+        assert ei.value.code == -4
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama8b", "wholedoc"])
