@@ -59,7 +59,9 @@ enum {
   FC_ERR_UNSUPPORTED = -4, /* head dim or group size not compiled in */
   FC_ERR_WORKSPACE = -5,   /* workspace too small, or view not bound */
   FC_ERR_HIP = -6,         /* a HIP runtime call failed */
-  FC_ERR_CAPACITY = -7     /* output array too small; *n_out holds the need */
+  FC_ERR_CAPACITY = -7,    /* output array too small; *n_out holds the need */
+  FC_ERR_INTERNAL = -8     /* a table the library built failed its own bounds
+                              check before upload (a library bug) */
 };
 
 /* fwd pass modes */
@@ -193,6 +195,26 @@ int fc_view_get_info(fc_view view, fc_view_info* out);
 int fc_view_export(fc_view view, int32_t* q_gpos, int32_t* recv_gpos, int32_t* seg_doc,
                    int32_t* q_cu_docseg, int32_t* recv_cu, int32_t* pieces, int32_t* lim,
                    int32_t* fwd_local, int32_t* fwd_recv, int32_t* fwd_fused, int32_t* bwd);
+
+/* The launch tables a view's kernels read, copied from exactly the blob
+ * fc_view_bind uploads (for checks; any pointer may be NULL):
+ *   fwd_local/fwd_recv/fwd_fused[n*8]  the forward items of fc_view_export,
+ *                                      in launch order (largest first);
+ *   bwd_launch[n_bwd_launch*8]         (k0, k1, q0, q1, qfull, src, seg, slot):
+ *                                      the backward items, key tiles seen by
+ *                                      many query tiles split into parts over
+ *                                      consecutive query tiles, each part
+ *                                      writing partial slot `slot` (-1: no
+ *                                      split), largest first;
+ *   bwd_reduce[n_bwd_reduce*8]         (src, k0, k1, first slot, slot count,
+ *                                      0, 0, 0) per split key tile;
+ *   bwd_qfirst[n_bwd_launch*(bn_bwd/32)] per launch item and 32-key wave
+ *                                      (keys k0 + 32w ...): the first query
+ *                                      row in [q0, q1) that sees key k0 + 32w
+ *                                      (q1 if none). */
+int fc_view_export_launch(fc_view view, int32_t* fwd_local, int32_t* fwd_recv,
+                          int32_t* fwd_fused, int32_t* bwd_launch, int32_t* bwd_reduce,
+                          int32_t* bwd_qfirst);
 
 /* Upload the view's tables into `dev_meta` (device, >= meta_bytes, 256-byte
  * aligned) on `stream` and remember that buffer for later kernel calls. */

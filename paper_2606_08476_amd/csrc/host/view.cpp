@@ -190,6 +190,46 @@ void View::build_bwd_launch() {
   }
 }
 
+// Every index the kernels will take from the tables, checked against the
+// extents they index (t_q, t_recv, the slot count) before anything is
+// uploaded: a table out of range is a library bug, reported as such rather
+// than handed to a kernel.
+int View::check_tables() const {
+  const int32_t tq = t_q(), tr = t_recv();
+  auto bad = [](const char* what, size_t i) {
+    return fail(FC_ERR_INTERNAL, std::string("internal: ") + what + " entry " + std::to_string(i) +
+                                     " out of range");
+  };
+  for (const auto* list : {&fwd_local, &fwd_recv, &fwd_fused}) {
+    for (size_t i = 0; i < list->size() / 8; ++i) {
+      const int32_t* it = &(*list)[8 * i];
+      if (!(0 <= it[0] && it[0] < it[1] && it[1] <= tq && it[1] - it[0] <= bm_fwd))
+        return bad("forward item (queries)", i);
+      if (!(0 <= it[2] && it[2] <= it[3] && it[3] <= tr)) return bad("forward item (received)", i);
+      if (!(0 <= it[4] && it[4] <= it[5] && it[5] <= tq)) return bad("forward item (local)", i);
+    }
+  }
+  for (size_t i = 0; i < bwd_launch.size() / 8; ++i) {
+    const int32_t* it = &bwd_launch[8 * i];
+    const int32_t hi = it[5] ? tr : tq;
+    if (!((it[5] == 0 || it[5] == 1) && 0 <= it[0] && it[0] < it[1] && it[1] <= hi &&
+          it[1] - it[0] <= bn_bwd && 0 <= it[2] && it[2] < it[3] && it[3] <= tq &&
+          -1 <= it[7] && it[7] < n_bwd_slots))
+      return bad("backward launch item", i);
+  }
+  for (size_t i = 0; i < bwd_reduce.size() / 8; ++i) {
+    const int32_t* e = &bwd_reduce[8 * i];
+    const int32_t hi = e[0] ? tr : tq;
+    if (!((e[0] == 0 || e[0] == 1) && 0 <= e[1] && e[1] < e[2] && e[2] <= hi && 0 <= e[3] &&
+          0 < e[4] && e[3] + e[4] <= n_bwd_slots))
+      return bad("backward reduce entry", i);
+  }
+  if (bwd_qfirst.size() != bwd_launch.size() / 8 * size_t(bn_bwd / 32)) return bad("qfirst", 0);
+  for (size_t i = 0; i < lim.size(); ++i)
+    if (!(0 <= lim[i] && lim[i] <= tr)) return bad("receive limit", i);
+  return FC_OK;
+}
+
 void View::build_meta() {
   meta.clear();
   auto put = [&](const std::vector<int32_t>& v) {
@@ -296,6 +336,7 @@ int build_view(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_
     v.pairs_loc += seg_len * (seg_len + 1) / 2;
   }
   v.build_tiles();
+  if (int rc = v.check_tables()) return rc;
   v.build_meta();
   return FC_OK;
 }
@@ -370,6 +411,24 @@ int fc_view_export(fc_view view, int32_t* q_gpos, int32_t* recv_gpos, int32_t* s
   cp(fwd_recv, v.fwd_recv);
   cp(fwd_fused, v.fwd_fused);
   cp(bwd, v.bwd);
+  return FC_OK;
+}
+
+int fc_view_export_launch(fc_view view, int32_t* fwd_local, int32_t* fwd_recv,
+                          int32_t* fwd_fused, int32_t* bwd_launch, int32_t* bwd_reduce,
+                          int32_t* bwd_qfirst) {
+  clear_error();
+  if (!view) return fail(FC_ERR_INVALID_ARG, "view is null");
+  const View& v = *reinterpret_cast<View*>(view);
+  auto cp = [&](int32_t* dst, int64_t off, size_t n) {
+    if (dst) std::copy(v.meta.begin() + off, v.meta.begin() + off + int64_t(n), dst);
+  };
+  cp(fwd_local, v.off.fwd_local, v.fwd_local.size());
+  cp(fwd_recv, v.off.fwd_recv, v.fwd_recv.size());
+  cp(fwd_fused, v.off.fwd_fused, v.fwd_fused.size());
+  cp(bwd_launch, v.off.bwd_launch, v.bwd_launch.size());
+  cp(bwd_reduce, v.off.bwd_reduce, v.bwd_reduce.size());
+  cp(bwd_qfirst, v.off.bwd_qfirst, v.bwd_qfirst.size());
   return FC_OK;
 }
 

@@ -47,6 +47,7 @@ struct View {
   void build_tiles();
   void build_bwd_launch();
   void build_meta();
+  int check_tables() const;
 };
 
 int build_view(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_t n_shards,

@@ -21,14 +21,14 @@ FC_FUSED = 1
 
 ERRORS = {
     -1: "FC_ERR_INVALID_ARG", -2: "FC_ERR_PLAN", -3: "FC_ERR_SHAPE", -4: "FC_ERR_UNSUPPORTED",
-    -5: "FC_ERR_WORKSPACE", -6: "FC_ERR_HIP", -7: "FC_ERR_CAPACITY",
+    -5: "FC_ERR_WORKSPACE", -6: "FC_ERR_HIP", -7: "FC_ERR_CAPACITY", -8: "FC_ERR_INTERNAL",
 }
 
 # every function the header declares
 EXPORTS = [
     "fc_plan_per_doc", "fc_plan_per_seq", "fc_plan_whole_lpt", "fc_plan_hybrid", "fc_plan_validate",
     "fc_plan_stats", "fc_view_create", "fc_view_get_info", "fc_view_export", "fc_view_bind",
-    "fc_view_destroy", "fc_workspace_size", "fc_kv_gather", "fc_attn_fwd",
+    "fc_view_destroy", "fc_view_export_launch", "fc_workspace_size", "fc_kv_gather", "fc_attn_fwd",
     "fc_attn_fwd_partial", "fc_attn_fwd_partials", "fc_lse_merge", "fc_attn_bwd", "fc_bwd_preprocess",
     "fc_attn_bwd_pass", "fc_attn_bwd_dkdv", "fc_attn_bwd_dq", "fc_attn_bwd_noalloc", "fc_last_error",
 ]
@@ -95,6 +95,7 @@ def lib():
             "fc_view_get_info": [P, C.POINTER(ViewInfo)],
             "fc_view_export": [P] + [I32P] * 11,
             "fc_view_bind": [P, P, C.c_size_t, P],
+            "fc_view_export_launch": [P] + [I32P] * 6,
             "fc_workspace_size": [P, C.c_int32, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t),
                                   C.POINTER(C.c_size_t)],
             "fc_kv_gather": [P, P, P, C.c_int64, P, P, P, P, P],
@@ -245,6 +246,19 @@ class View:
         out["pieces"] = out["pieces"].reshape(-1, 5)
         for k in ("fwd_local", "fwd_recv", "fwd_fused", "bwd"):
             out[k] = out[k].reshape(-1, 8)
+        return out
+
+    def export_launch(self) -> dict:
+        """The launch tables exactly as uploaded (fc_view_export_launch)."""
+        i = self.info
+        nw = i["bn_bwd"] // 32
+        sizes = dict(fwd_local=8 * i["n_fwd_local"], fwd_recv=8 * i["n_fwd_recv"],
+                     fwd_fused=8 * i["n_fwd_fused"], bwd_launch=8 * i["n_bwd_launch"],
+                     bwd_reduce=8 * i["n_bwd_reduce"], bwd_qfirst=nw * i["n_bwd_launch"])
+        arrs = {k: np.zeros(max(1, v), dtype=np.int32) for k, v in sizes.items()}
+        _check(lib().fc_view_export_launch(self.handle, *[arrs[k].ctypes.data_as(I32P) for k in sizes]))
+        out = {k: arrs[k][:sizes[k]].reshape(-1, 8) for k in sizes if k != "bwd_qfirst"}
+        out["bwd_qfirst"] = arrs["bwd_qfirst"][:sizes["bwd_qfirst"]].reshape(-1, nw)
         return out
 
     def bind(self, device="cuda", buf=None):

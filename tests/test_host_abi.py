@@ -235,11 +235,11 @@ def test_empty_rank_view():
     v.close()
 
 
-def test_backward_launch_split_covers_the_map():
-    """The backward launch list splits long key tiles into query-range parts
-    (aligned to query tiles) that together cover the canonical item exactly,
-    each split tile with a reduce entry naming consecutive partial slots."""
-    lib = F.lib()
+def test_backward_workspace_holds_the_partial_slots():
+    """The dK/dV workspace is exactly the split key tiles' partial slots (two
+    fp32 tiles of 128 keys x d per KV head each), and the Whole-Doc shard
+    does split tiles. The split itself is checked against the tile map by
+    brute force in test_launch_tables.py."""
     for name in ("wholedoc", "llama8b"):
         w = synth.WORKLOADS[name]
         cu = synth.cu_seqlens(synth.doc_lengths(name))
@@ -247,28 +247,9 @@ def test_backward_launch_split_covers_the_map():
         rank = int(np.argmax(P.stats(cu, w.cp, plan, 1, 1)["work"]))
         v = F.View(cu, plan, w.cp, rank, w.hq, w.hkv, w.d)
         i = v.info
-        view = V.rank_view(cu, plan, rank)
-        canon = V.bwd_items(view, i["bm_bwd"], i["bn_bwd"])
-        # rebuild the launch list through the device table layout is internal; check via sizes
-        # and by re-deriving the split from the documented rule
-        G = w.hq // w.hkv
-        nt = (canon[:, 3] - canon[:, 2] + i["bm_bwd"] - 1) // i["bm_bwd"]
-        total = int(nt.sum()) * G
-        cap = max(16, -(-total * w.hkv // 512))
-        parts = np.maximum(1, -(-(nt * G) // cap))
-        assert i["n_bwd_reduce"] == int((parts > 1).sum())
-        n_launch = 0
-        slots = 0
-        for n_t, p in zip(nt.tolist(), parts.tolist()):
-            per = -(-n_t // p)
-            k = -(-n_t // per)
-            n_launch += k
-            if p > 1:
-                slots += k
-        assert i["n_bwd_launch"] == n_launch and i["n_bwd_slots"] == slots
-        f, b, k = v.workspace_size()
-        assert k == 2 * slots * w.hkv * 128 * w.d * 4
+        slots = int((v.export_launch()["bwd_launch"][:, 7] >= 0).sum())
+        assert slots == i["n_bwd_slots"]
+        assert v.workspace_size()[2] == 2 * slots * w.hkv * 128 * w.d * 4
         if name == "wholedoc":
             assert slots > 0
         v.close()
-
