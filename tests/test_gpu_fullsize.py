@@ -178,3 +178,52 @@ def test_full_size(name, seed, dev):
         (f" (huge segments {huge} {'KV head 0' if seed == 0 else 'skipped'})" if huge else ""))
     assert err["o"] <= TOL and err["dq"] <= TOL and err["lse"] <= LSE_TOL
     assert err["dk"] <= DKDV_MARGIN and err["dv"] <= DKDV_MARGIN
+
+
+def test_granularity_shapes(dev):
+    """The shard-granularity study's full-size shapes, Llama-3-8B heads,
+    through the bench's launch sequence:
+    * 16 documents of 8192 tokens under the per-sequence plan at N = 8
+      (rank 0 holds documents 0 and 15 whole): every row and key of KV head
+      0 and its query heads;
+    * one 131072-token document held whole by one rank: O, LSE and dQ on 64
+      sampled rows and on the last 256 rows (all heads), dK and dV on the
+      last 256 keys (no other row sees them, so the oracle restricted to
+      those rows is exact for them)."""
+    case = _cases.make_case("docs16x8k_per_seq8", "llama8b", lens=[8192] * 16, cp=8,
+                            plan="per_seq", rank=0)
+    say(f"[gpu-full] {case.name}: t_q {case.oview.q_gpos.size}, t_recv {case.oview.recv_gpos.size}")
+    x = _cases.inputs(case)
+    v, out = bench_sequence(case, x, dev)
+    v.close()
+    err, huge = compare(case, x, out, huge_group=True)
+    assert huge == [0, 1]
+    say(f"[gpu-full] {case.name}: " + " ".join(f"{k} {e:.3e}" for k, e in err.items()))
+    assert max(err["o"], err["dq"], err["dk"], err["dv"]) <= TOL and err["lse"] <= LSE_TOL
+
+    case = _cases.make_case("one_doc_128k", "llama8b", lens=[131072], cp=1, plan="whole_lpt", rank=0)
+    x = _cases.inputs(case)
+    v, out = bench_sequence(case, x, dev)
+    v.close()
+    say(f"[gpu-full] {case.name}: GPU done")
+    T = 131072
+    rng = np.random.default_rng(5)
+    tail = np.arange(T - 256, T)
+    rows = np.unique(np.concatenate([rng.choice(T - 256, size=64, replace=False), tail]))
+    ov = case.oview
+    t0 = time.time()
+    dq_r, dk_r, dv_r, O_r, L_r = A.attention_bwd(case.cu, ov.q_gpos, x["q"], ov.q_gpos, x["k_loc"],
+                                                 x["v_loc"], x["do"], rows=rows,
+                                                 dtype=torch.float32, with_fwd=True)
+    rr = torch.as_tensor(rows)
+    eo = float((out["o"][rr].double() - O_r[rr].double()).abs().max())
+    lr = L_r[:, rr].double()
+    el = float(((out["lse"][:, rr].double() - lr).abs() / lr.abs().clamp_min(1)).max())
+    # dQ of the tail rows only: the sampled rows' dQ is complete too
+    eq = float((out["dq"][rr].double() - dq_r[rr].double()).abs().max())
+    tt = torch.as_tensor(tail)
+    ek = float((out["dk_loc"][tt].double() - dk_r[tt].double()).abs().max())
+    ev = float((out["dv_loc"][tt].double() - dv_r[tt].double()).abs().max())
+    say(f"[gpu-full] {case.name}: {rows.size} rows (oracle {time.time() - t0:.1f} s): O {eo:.3e} "
+        f"LSE {el:.3e} dQ {eq:.3e}; last 256 keys: dK {ek:.3e} dV {ev:.3e}")
+    assert max(eo, eq, ek, ev) <= TOL and el <= LSE_TOL
