@@ -300,8 +300,13 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
         if ((u + 1) * ES == 8) sa[0] = pack8(dpacc, 0);
         if ((u + 1) * ES == 16) sa[1] = pack8(dpacc, 8);
         if (u == 2 * DB - 1 && split) {
-          residual({pack8_lo(sacc, 0), pack8_lo(sacc, 8)}, OO, dv);
-          residual({pack8_lo(dpacc, 0), pack8_lo(dpacc, 8)}, QO, dk);
+          // (P and dS through opaque copies: the compiler would otherwise
+          // share their bf16 conversions with the packs above, converting
+          // element by element on the common path for this rare one)
+          f32x16 pf = sacc, sf = dpacc;
+          asm volatile("" : "+v"(pf), "+v"(sf));
+          residual({pack8_lo(pf, 0), pack8_lo(pf, 8)}, OO, dv);
+          residual({pack8_lo(sf, 0), pack8_lo(sf, 8)}, QO, dk);
         }
       } else {
         const int u = n - 2 * KS - 2 * DB, kh = u / DB, db = u % DB;
