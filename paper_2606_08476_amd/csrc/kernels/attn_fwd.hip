@@ -4,9 +4,10 @@
 // with a received key range (no mask inside it, FlashCP Sec. 3.2: every
 // query of a piece sees the same received prefix) and a local key range
 // (intra-document causal, Sec. 2.1) -- for `heads_per_tile` query heads of
-// one KV head. Each wave owns 32 query rows of one head. Key tiles of 64
-// keys are double-buffered in LDS and shared by the waves (and so by the
-// heads of the group); later tiles are copied from HBM straight into LDS
+// one KV head. Each wave owns 32/heads_per_tile query rows of every one of
+// those heads (a query per lane). Key tiles of 64 keys are double-buffered
+// in LDS and shared by the waves (and so by the heads of the group); later
+// tiles are copied from HBM straight into LDS
 // (asynchronous loads, no staging registers) while the current one is
 // computed, and the loop is software-pipelined across tiles (the scores of
 // the next tile are computed beside the softmax of the current one):
@@ -44,7 +45,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   constexpr bool FINAL = OUT == kOutFinal, MERGED = OUT == kOutMerged;
   constexpr bool PAIRED = OUT == kOutPaired || MERGED;
   constexpr int BN = 64;        // keys per tile
-  constexpr int WPH = 4 / HPW;  // waves per query head
+  constexpr int RPW = 32 / HPW;  // query rows per wave and head
   constexpr int KS = D / 16;    // MFMA k-steps over the head dim
   constexpr int DB = D / 32;    // 32-wide output blocks of the head dim
   constexpr float kLazy = 8.0f; // log2 headroom before rescaling
@@ -70,9 +71,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int q0 = it[0], q1 = it[1], r0 = it[2], r1 = it[3], l0 = it[4], l1 = it[5];
   const int ldiag = it[6];
 
-  const int h = kvh * p.group + hc * HPW + wave / WPH;
-  const int qrow = q0 + (wave % WPH) * 32 + (lane & 31);
+  // lane -> (query row, head): a wave takes RPW consecutive rows of each of
+  // the HPW heads, so a short query range leaves whole waves without rows
+  // (they skip the products and only help with the copies and barriers)
+  // instead of padding every head's rows to 32
+  const int l31 = lane & 31;
+  const int h = kvh * p.group + hc * HPW + l31 / RPW;
+  const int qrow = q0 + wave * RPW + l31 % RPW;
   const bool qvalid = qrow < q1;
+  const bool active = q0 + wave * RPW < q1;  // wave-uniform
   const float c = p.scale_log2;
 
   // key tiles: first the received range, then the local range
@@ -212,7 +219,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   __syncthreads();
   f32x16 sa[2], sb[2];  // scores of the current and of the next tile
   float mxa = -INFINITY, mxb = -INFINITY;
-  if (n_t > 0) {
+  if (n_t > 0 && active) {
     scores(sa, 0);
     mask(sa, 0);
     mxa = row_max(sa);
@@ -241,79 +248,81 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     if (j + 1 < n_t) fetch(j + 1, (3 - PAR) * TILE, true);   // V of tile j+1
     if (j + 2 < n_t) fetch(j + 2, PAR * TILE, false);        // K of tile j+2
     if (PAIRED && j == n_r) switch_source();
-    // a row's output is rescaled only when its maximum grows by more than
-    // the headroom; rows that do not grow keep their maximum and scale by 1
-    const bool grow = mxc > m + kLazy;  // implies mxc > m
-    if (__any(grow)) {
-      const float alpha =
-          !grow ? 1.f : m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mxc);
-      m = grow ? mxc : m;
-      lsum *= alpha;
+    if (active) {
+      // a row's output is rescaled only when its maximum grows by more than
+      // the headroom; rows that do not grow keep their maximum and scale by 1
+      const bool grow = mxc > m + kLazy;  // implies mxc > m
+      if (__any(grow)) {
+        const float alpha =
+            !grow ? 1.f : m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mxc);
+        m = grow ? mxc : m;
+        lsum *= alpha;
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-    }
-    const float mref = m == -INFINITY ? 0.f : m;
+          for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+      }
+      const float mref = m == -INFINITY ? 0.f : m;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) pk[ks] = opaque(pk[ks]);
+      for (int ks = 0; ks < KS; ++ks) pk[ks] = opaque(pk[ks]);
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      pv[db][0] = opaque(pv[db][0]);
-      pv[db][1] = opaque(pv[db][1]);
-    }
+      for (int db = 0; db < DB; ++db) {
+        pv[db][0] = opaque(pv[db][0]);
+        pv[db][1] = opaque(pv[db][1]);
+      }
 
-    bf16x8 ring[3], pb[4];
-    // operand of slot n: K rows of tile j+1 (score slots), V^T of tile j
-    // (PV slots)
-    auto rd = [&](int n) {
-      if (n < 2 * KS) {
-        ring[n % 3] = lds_b128(smem, pk[n / 2], KN + (n % 2) * 64 * D);
-      } else {
-        const int u = n - 2 * KS, kk = u / DB, db = u % DB;
-        const uint32_t ro = VC + kk * 32 * D;  // rows 16*kk..
-        ring[n % 3] = cat8(lds_tr(smem, pv[db][0], ro), lds_tr(smem, pv[db][1], ro));
-      }
-    };
-    float ps = 0.f, mx = -INFINITY;
-    sn[0] = zero16();
-    sn[1] = zero16();
-    rd(0);
-    rd(1);
-    static_for<0, NS>([&](auto nc) {
-      constexpr int n = decltype(nc)::value;
-      if (n + 2 < NS) rd(n + 2);
-      if constexpr (n < 2 * KS) {
-        sn[n % 2] = mfma32(ring[n % 3], qreg[n / 2], sn[n % 2]);
+      bf16x8 ring[3], pb[4];
+      // operand of slot n: K rows of tile j+1 (score slots), V^T of tile j
+      // (PV slots)
+      auto rd = [&](int n) {
+        if (n < 2 * KS) {
+          ring[n % 3] = lds_b128(smem, pk[n / 2], KN + (n % 2) * 64 * D);
+        } else {
+          const int u = n - 2 * KS, kk = u / DB, db = u % DB;
+          const uint32_t ro = VC + kk * 32 * D;  // rows 16*kk..
+          ring[n % 3] = cat8(lds_tr(smem, pv[db][0], ro), lds_tr(smem, pv[db][1], ro));
+        }
+      };
+      float ps = 0.f, mx = -INFINITY;
+      sn[0] = zero16();
+      sn[1] = zero16();
+      rd(0);
+      rd(1);
+      static_for<0, NS>([&](auto nc) {
+        constexpr int n = decltype(nc)::value;
+        if (n + 2 < NS) rd(n + 2);
+        if constexpr (n < 2 * KS) {
+          sn[n % 2] = mfma32(ring[n % 3], qreg[n / 2], sn[n % 2]);
 #pragma unroll
-        for (int e = n * EX; e < (n + 1) * EX; ++e) {
-          const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e / 16][e % 16], c, -mref));
-          sc[e / 16][e % 16] = x;
-          ps += x;
-          if (e % 8 == 7) {
-            pb[e / 8] = pack8(sc[e / 16], 8 * ((e / 8) & 1));
-            // complete here: keeps the exponentials in the score slots
-            // rather than sunk past the masking branch into the PV slots
-            asm volatile("" ::"v"(pb[e / 8]));
+          for (int e = n * EX; e < (n + 1) * EX; ++e) {
+            const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e / 16][e % 16], c, -mref));
+            sc[e / 16][e % 16] = x;
+            ps += x;
+            if (e % 8 == 7) {
+              pb[e / 8] = pack8(sc[e / 16], 8 * ((e / 8) & 1));
+              // complete here: keeps the exponentials in the score slots
+              // rather than sunk past the masking branch into the PV slots
+              asm volatile("" ::"v"(pb[e / 8]));
+            }
           }
-        }
-        if (n == 2 * KS - 1) {
-          lsum += ps;
-          asm volatile("" : "+v"(lsum));  // the row sum too, not sunk into the next step
-        }
-      } else {
-        constexpr int u = n - 2 * KS;
-        oacc[u % DB] = mfma32(ring[n % 3], pb[u / DB], oacc[u % DB]);
-        if constexpr (u == MX - 1) mask(sn, j + 1);
-        if constexpr (u >= MX) {
+          if (n == 2 * KS - 1) {
+            lsum += ps;
+            asm volatile("" : "+v"(lsum));  // the row sum too, not sunk into the next step
+          }
+        } else {
+          constexpr int u = n - 2 * KS;
+          oacc[u % DB] = mfma32(ring[n % 3], pb[u / DB], oacc[u % DB]);
+          if constexpr (u == MX - 1) mask(sn, j + 1);
+          if constexpr (u >= MX) {
 #pragma unroll
-          for (int e = (u - MX) * MPS; e < (u - MX + 1) * MPS && e < 32; ++e)
-            mx = fmaxf(mx, sn[e / 16][e % 16]);
+            for (int e = (u - MX) * MPS; e < (u - MX + 1) * MPS && e < 32; ++e)
+              mx = fmaxf(mx, sn[e / 16][e % 16]);
+          }
+          if constexpr (u == 4 * DB - 1) mxn = max_halves(mx) * c;
         }
-        if constexpr (u == 4 * DB - 1) mxn = max_halves(mx) * c;
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
     wait_async();
     __syncthreads();
   };

@@ -32,7 +32,7 @@ struct DqLds {
 template <int D, int HPW>
 __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
   constexpr int BN = 64;
-  constexpr int WPH = 4 / HPW;
+  constexpr int RPW = 32 / HPW;  // query rows per wave and head
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
   constexpr uint32_t TILE = BN * D * 2;  // bytes of one K or V tile
@@ -49,9 +49,13 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
   const int q0 = it[0], q1 = it[1], r0 = it[2], r1 = it[3], l0 = it[4], l1 = it[5];
   const int ldiag = it[6];
 
-  const int h = kvh * p.group + hc * HPW + wave / WPH;
-  const int qrow = q0 + (wave % WPH) * 32 + (lane & 31);
+  // lane -> (query row, head) as in the forward: RPW rows of each of the
+  // HPW heads per wave; a wave with no row skips the products
+  const int l31 = lane & 31;
+  const int h = kvh * p.group + hc * HPW + l31 / RPW;
+  const int qrow = q0 + wave * RPW + l31 % RPW;
   const bool qvalid = qrow < q1;
+  const bool active = q0 + wave * RPW < q1;  // wave-uniform
   const float sl2 = p.scale * kLog2e;
 
   const int n_r = (r1 - r0 + BN - 1) / BN;
@@ -119,83 +123,85 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
     const bool rs = j < n_r;
     const int k0 = rs ? r0 + j * BN : l0 + (j - n_r) * BN;
     const int hi = rs ? r1 : l1;
+    if (active) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) pr[ks] = opaque(pr[ks]);
+      for (int ks = 0; ks < KS; ++ks) pr[ks] = opaque(pr[ks]);
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      pt[db][0] = opaque(pt[db][0]);
-      pt[db][1] = opaque(pt[db][1]);
-    }
-    // key k0 + 4*half + c (c = 32*mb + 8*(i/4) + i%4 for register i) is seen
-    // iff c < rel: keys past the range, and later keys on diagonal tiles,
-    // give P = 0. Only edge tiles (diagonal, or running past the range)
-    // mask, in one branch before each half's dS.
-    const bool diag = !rs && k0 >= ldiag;
-    const int rel = (diag ? min(hi, qrow + 1) : hi) - k0 - 4 * half;
-    const bool edge = diag || k0 + BN > hi;
+      for (int db = 0; db < DB; ++db) {
+        pt[db][0] = opaque(pt[db][0]);
+        pt[db][1] = opaque(pt[db][1]);
+      }
+      // key k0 + 4*half + c (c = 32*mb + 8*(i/4) + i%4 for register i) is seen
+      // iff c < rel: keys past the range, and later keys on diagonal tiles,
+      // give P = 0. Only edge tiles (diagonal, or running past the range)
+      // mask, in one branch before each half's dS.
+      const bool diag = !rs && k0 >= ldiag;
+      const int rel = (diag ? min(hi, qrow + 1) : hi) - k0 - 4 * half;
+      const bool edge = diag || k0 + BN > hi;
 
-    f32x16 s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
-    bf16x8 ring[3], sb[4];
-    auto rd = [&](int n) {
-      bf16x8& a = ring[n % 3];
-      if (n < 4 * KS) {  // K rows (S) or V rows (dP)
-        const int ks = n % KS, mb = (n / KS) & 1;
-        a = lds_b128(smem, pr[ks], (n < 2 * KS ? KO : VO) + mb * 64 * D);
-      } else {  // K^T for dQ
-        const int u = n - 4 * KS, kk = u / DB, db = u % DB;
-        const uint32_t ro = KO + kk * 32 * D;
-        a = cat8(lds_tr(smem, pt[db][0], ro), lds_tr(smem, pt[db][1], ro));
-      }
-    };
-    auto pexp = [&](int mb, int i) {
-      s[mb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], sl2, -lse2));
-    };
-    auto mask = [&](int mb) {
-      if (edge) {
+      f32x16 s[2] = {zero16(), zero16()}, dp[2] = {zero16(), zero16()};
+      bf16x8 ring[3], sb[4];
+      auto rd = [&](int n) {
+        bf16x8& a = ring[n % 3];
+        if (n < 4 * KS) {  // K rows (S) or V rows (dP)
+          const int ks = n % KS, mb = (n / KS) & 1;
+          a = lds_b128(smem, pr[ks], (n < 2 * KS ? KO : VO) + mb * 64 * D);
+        } else {  // K^T for dQ
+          const int u = n - 4 * KS, kk = u / DB, db = u % DB;
+          const uint32_t ro = KO + kk * 32 * D;
+          a = cat8(lds_tr(smem, pt[db][0], ro), lds_tr(smem, pt[db][1], ro));
+        }
+      };
+      auto pexp = [&](int mb, int i) {
+        s[mb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], sl2, -lse2));
+      };
+      auto mask = [&](int mb) {
+        if (edge) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-          s[mb][i] = 32 * mb + 8 * (i >> 2) + (i & 3) < rel ? s[mb][i] : 0.f;
-      }
-    };
-    auto dsv = [&](int mb, int i) { dp[mb][i] = s[mb][i] * (dp[mb][i] - del); };
-    rd(0);
-    rd(1);
-    static_for<0, NS>([&](auto nc) {
-      constexpr int n = decltype(nc)::value;
-      if (n + 2 < NS) rd(n + 2);
-      const bf16x8& a = ring[n % 3];
-      if (n < 2 * KS) {
-        const int ks = n % KS, mb = n / KS;
-        s[mb] = mfma32(a, qreg[ks], s[mb]);
-        if (mb == 1)
+          for (int i = 0; i < 16; ++i)
+            s[mb][i] = 32 * mb + 8 * (i >> 2) + (i & 3) < rel ? s[mb][i] : 0.f;
+        }
+      };
+      auto dsv = [&](int mb, int i) { dp[mb][i] = s[mb][i] * (dp[mb][i] - del); };
+      rd(0);
+      rd(1);
+      static_for<0, NS>([&](auto nc) {
+        constexpr int n = decltype(nc)::value;
+        if (n + 2 < NS) rd(n + 2);
+        const bf16x8& a = ring[n % 3];
+        if (n < 2 * KS) {
+          const int ks = n % KS, mb = n / KS;
+          s[mb] = mfma32(a, qreg[ks], s[mb]);
+          if (mb == 1)
 #pragma unroll
-          for (int e = ks * EP; e < (ks + 1) * EP; ++e) pexp(0, e);
-      } else if (n < 4 * KS) {
-        const int ks = n % KS, mb = (n - 2 * KS) / KS;
-        dp[mb] = mfma32(a, oreg[ks], dp[mb]);
-        if (mb == 1 && ks == 0) mask(0);
-        if (mb == 0) {
+            for (int e = ks * EP; e < (ks + 1) * EP; ++e) pexp(0, e);
+        } else if (n < 4 * KS) {
+          const int ks = n % KS, mb = (n - 2 * KS) / KS;
+          dp[mb] = mfma32(a, oreg[ks], dp[mb]);
+          if (mb == 1 && ks == 0) mask(0);
+          if (mb == 0) {
 #pragma unroll
-          for (int e = ks * EP; e < (ks + 1) * EP; ++e) pexp(1, e);
+            for (int e = ks * EP; e < (ks + 1) * EP; ++e) pexp(1, e);
+          } else {
+#pragma unroll
+            for (int e = ks * EP; e < (ks + 1) * EP; ++e) dsv(0, e);
+            if ((ks + 1) * EP == 8) sb[0] = pack8(dp[0], 0);
+            if ((ks + 1) * EP == 16) sb[1] = pack8(dp[0], 8);
+          }
         } else {
+          const int u = n - 4 * KS, kk = u / DB, db = u % DB;
+          dq[db] = mfma32(a, sb[kk], dq[db]);
+          if (u == 0) mask(1);
+          if (u < 2 * DB) {
 #pragma unroll
-          for (int e = ks * EP; e < (ks + 1) * EP; ++e) dsv(0, e);
-          if ((ks + 1) * EP == 8) sb[0] = pack8(dp[0], 0);
-          if ((ks + 1) * EP == 16) sb[1] = pack8(dp[0], 8);
+            for (int e = u * EQ; e < (u + 1) * EQ; ++e) dsv(1, e);
+            if ((u + 1) * EQ == 8) sb[2] = pack8(dp[1], 0);
+            if ((u + 1) * EQ == 16) sb[3] = pack8(dp[1], 8);
+          }
         }
-      } else {
-        const int u = n - 4 * KS, kk = u / DB, db = u % DB;
-        dq[db] = mfma32(a, sb[kk], dq[db]);
-        if (u == 0) mask(1);
-        if (u < 2 * DB) {
-#pragma unroll
-          for (int e = u * EQ; e < (u + 1) * EQ; ++e) dsv(1, e);
-          if ((u + 1) * EQ == 8) sb[2] = pack8(dp[1], 0);
-          if ((u + 1) * EQ == 16) sb[3] = pack8(dp[1], 8);
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
     wait_async();
     __syncthreads();
   };
