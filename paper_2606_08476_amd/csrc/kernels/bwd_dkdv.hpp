@@ -5,8 +5,11 @@
 // received) and one KV head; wave w owns keys 32w..32w+31, so dK and dV for
 // the tile accumulate in registers, summed over every query head of the
 // group (grouped-query attention) and every query tile that sees the keys.
-// K sits in LDS, V in registers. The (query head, 32-query tile) iterations
-// are software-pipelined: the next tile's Q and dO are copied from HBM
+// K sits in LDS, V in registers. An iteration takes 32 (query row, query
+// head) pairs: 32/HPI consecutive query rows of each of HPI heads of the
+// group (HPI = 4 when the group allows it), so the last, short block of a
+// query range pads to 32/HPI rows rather than 32. The iterations are
+// software-pipelined: the next block's Q and dO are copied from HBM
 // straight into a second LDS buffer (asynchronous loads) while the current
 // one is computed. Per iteration:
 //   S  = Q K^T, dP = dO V^T     MFMA (Q, dO, K from LDS, V from registers);
@@ -42,11 +45,13 @@ struct DkdvLds {
 };
 
 // One workgroup's key tile (workgroup index b); smem: DkdvLds<D, DQ>::bytes
-// of shared memory.
-template <int D, bool DQ = false>
+// of shared memory. HPI (1, 2 or 4) must divide the group size.
+template <int D, bool DQ = false, int HPI = 1>
 __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem) {
   constexpr int BN = 128;       // keys per workgroup
-  constexpr int BM = 32;        // queries per iteration
+  constexpr int BM = 32;        // (query row, head) pairs per iteration
+  constexpr int RPI = BM / HPI; // query rows per iteration and head
+  static_assert(HPI == 1 || HPI == 2 || HPI == 4, "heads per iteration");
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
   constexpr uint32_t KT = BN * D * 2;  // bytes of the key tile
@@ -97,14 +102,17 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
       vreg[ks] = kvalid ? *reinterpret_cast<const bf16x8*>(vp + 16 * ks) : zero8();
   }
 
-  const int ntile = (q1 - q0 + BM - 1) / BM;
-  const int n_it = ntile * p.group;
+  const int ntile = (q1 - q0 + RPI - 1) / RPI;
+  const int n_it = ntile * (p.group / HPI);
 
-  // iteration i covers query head kvh * group + i / ntile and query tile
-  // i % ntile; both are carried from one iteration to the next (no integer
-  // division per iteration)
-  int cur_t = 0, cur_h = 0;   // query tile and head of the current iteration
-  int nxt_t = 0, nxt_h = 0;   // query tile and head of the next copy
+  // iteration i covers query heads kvh * group + HPI * (i / ntile) + 0 ..
+  // HPI-1 and query rows q0 + RPI * (i % ntile) + 0 .. RPI-1; block and head
+  // set are carried from one iteration to the next (no integer division
+  // per iteration). Pair m (0..31) of an iteration is row m % RPI of head
+  // m / RPI: the row order of the Q/dO tiles, of the LSE, delta and limit
+  // slots and of the MFMA rows.
+  int cur_t = 0, cur_h = 0;   // row block and head set of the current iteration
+  int nxt_t = 0, nxt_h = 0;   // row block and head set of the next copy
   auto advance = [&]() {
     if (++nxt_t == ntile) {
       nxt_t = 0;
@@ -114,22 +122,24 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
 
   // next iteration: Q/dO tiles, LSE, D and receive limits, all copied from
   // HBM straight into LDS (rows past q1 repeat the last query; masked)
-  const TileLoader<D, BM> ldq(p.hq * D);
+  const TileLoader<D, BM, 256, RPI> ldq(p.hq * D, D);
   auto fetch = [&](int hh, int tt, int buf) {
-    const int h = kvh * p.group + hh;
-    const int t0 = q0 + tt * BM;
+    const int h = kvh * p.group + hh * HPI;
+    const int t0 = q0 + tt * RPI;
     const size_t base = (size_t(t0) * p.hq + h) * D;
     const uint32_t sb = lds_addr(smem);
     ldq.load_at(sb + (buf ? OQ1 : OQ0), p.q + base, q1 - t0);
     ldq.load_at(sb + (buf ? OO1 : OO0), p.dout + base, q1 - t0);
-    const uint32_t qoff = 4u * uint32_t(min(t0 + (lane & 31), q1 - 1));
+    const int m = lane & 31;
+    const uint32_t roff = 4u * uint32_t(min(t0 + m % RPI, q1 - 1));
+    const uint32_t qoff = roff + 4u * uint32_t(m / RPI) * uint32_t(p.t_q);
     const uint32_t sm = sb + 768u * buf;
     if (wave == 0)
       lds_copy4(p.lse + (size_t)h * p.t_q, qoff, sm);
     else if (wave == 1)
       lds_copy4(p.delta + (size_t)h * p.t_q, qoff, sm + 256);
     else if (wave == 2 && src)
-      lds_copy4(p.lim, qoff, sm + 512);
+      lds_copy4(p.lim, roff, sm + 512);
   };
 
   // per-lane LDS byte offsets (swizzled tiles): row reads of a 32-row block
@@ -147,7 +157,6 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   }
   const bool kfull = k1 - k0 == BN;
   const float sl2 = p.scale * kLog2e;
-  // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
 
   if (n_it > 0) fetch(0, 0, 0);
   advance();
@@ -182,8 +191,9 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   auto tile = [&](int t0, auto bufc, bool edge) {
     constexpr int B = decltype(bufc)::value;
     constexpr uint32_t QO = B ? OQ1 : OQ0, OO = B ? OO1 : OO0, SO = 768u * B;
-    // masks: this lane's key against query rows t0 + 4*half + cq, cq = 8g + j
-    // (register 4g + j): rows cq < hiq exist; on a local diagonal the key is
+    // masks: this lane's key against query rows t0 + 4*half + cq, cq =
+    // (8g) % RPI + j (register 4g + j, pair 8g + 4*half + j): rows cq < hiq
+    // exist; on a local diagonal the key is
     // seen by rows cq >= lo; on a received diagonal by rows whose receive
     // limit exceeds the key index
     // (this lane's key is recomputed here from an opaque lane index rather
@@ -230,7 +240,7 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
         m4[g] = *reinterpret_cast<const int4*>(smem + SO + 512 + 4 * (8 * g + 4 * half));
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int g = e >> 2, j = e & 3, cq = 8 * g + j;
+        const int g = e >> 2, j = e & 3, cq = (8 * g) % RPI + j;
         // (local tiles never copy limits into LDS: what is there is stale
         // and must not be compared)
         const int lim = !src ? 0x7fffffff
@@ -372,8 +382,10 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
     const int cb = wave % DB;
     const uint32_t ln = opaque(uint32_t(lane));
     const int hf = ln >> 5;
-    // C layout: register i is query row 8*(i/4) + 4h + i%4, column 32cb +
-    // lane%32; each register's 64 lanes cover two 128-byte row segments.
+    // C layout: register i is pair 8*(i/4) + 4h + i%4 (query row
+    // (8*(i/4)) % RPI + 4h + i%4 of head set member (8*(i/4)) / RPI), column
+    // 32cb + lane%32; each register's 64 lanes cover two 128-byte row
+    // segments.
     // Addresses: a wave-uniform row base per register (scalar registers)
     // plus one 32-bit lane offset shared by all sixteen.
     // (the stride goes through an empty asm per iteration, so the row bases
@@ -382,11 +394,11 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
     uint32_t rs = uint32_t(p.hq) * D;
     asm volatile("" : "+s"(rs));
     const uint32_t loff = uint32_t(4 * hf) * rs + 32u * cb + (ln & 31);
-    float* const base = p.dq + (size_t(t0) * p.hq + kvh * p.group + hh) * D;
+    float* const base = p.dq + (size_t(t0) * p.hq + kvh * p.group + hh * HPI) * D;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int r0 = 8 * (i >> 2) + (i & 3);
-      float* const bi = base + size_t(r0) * rs;
+      const int r0 = (8 * (i >> 2)) % RPI + (i & 3), hm = (8 * (i >> 2)) / RPI;
+      float* const bi = base + size_t(r0) * rs + hm * D;
       if (t0 + r0 + 4 * hf < q1) atomicAdd(bi + loff, p.scale * qacc[i]);
     }
   };
@@ -397,16 +409,16 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   // where no row sees any of them (the tile ends before qfirst, or the keys
   // are past the range); masked otherwise.
   auto step = [&](int i_, auto bufc) {
-    const int t0 = q0 + cur_t * BM, hh = cur_h;
+    const int t0 = q0 + cur_t * RPI, hh = cur_h;
     if (i_ + 1 < n_it) fetch(nxt_h, nxt_t, decltype(bufc)::value ^ 1);
     cur_t = nxt_t;
     cur_h = nxt_h;
     advance();
     pr = opaque(pr);
     pt = opaque(pt);
-    const int tlast = min(t0 + BM, q1) - 1;
+    const int tlast = min(t0 + RPI, q1) - 1;
     const bool computed = !(kw >= k1 || tlast < qfirst);
-    if (computed) tile(t0, bufc, !(t0 >= qfull && t0 + BM <= q1 && kw + 32 <= k1));
+    if (computed) tile(t0, bufc, !(t0 >= qfull && t0 + RPI <= q1 && kw + 32 <= k1));
     f32x16 qacc;
     if constexpr (DQ) {
       if (!computed) put_ds(uint4{0u, 0u, 0u, 0u}, uint4{0u, 0u, 0u, 0u});

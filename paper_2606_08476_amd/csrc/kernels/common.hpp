@@ -258,25 +258,31 @@ __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
 
-// Asynchronous copies of ROWS x D bf16 tiles (rows row_stride elements apart
-// in HBM) into a swizzled LDS tile by a workgroup of NT threads. Each
-// thread's chunk byte offsets are computed once; a copy is then one uniform
-// base address plus those offsets. Rows at or past `nvalid` repeat row
-// nvalid-1 (finite data for masked rows, no read past the range).
-template <int D, int ROWS, int NT = 256>
+// Asynchronous copies of ROWS x D bf16 tiles into a swizzled LDS tile by a
+// workgroup of NT threads. Tile row r is HBM row (r % RPB) * row_stride +
+// (r / RPB) * block_stride elements from the base: RPB consecutive rows of
+// one block (one query head, say), then the next block (RPB = ROWS: one
+// block of rows row_stride apart). Each thread's chunk byte offsets are
+// computed once; a copy is then one uniform base address plus those
+// offsets. Rows whose index within their block is at or past `nvalid`
+// repeat row nvalid-1 of the same block (finite data for masked rows, no
+// read past the range).
+template <int D, int ROWS, int NT = 256, int RPB = ROWS>
 struct TileLoader {
   static constexpr int CH = D / 8;
   static constexpr int N = ROWS * CH / NT;
   static_assert((ROWS * CH) % NT == 0, "tile must be a multiple of NT chunks");
+  static_assert(ROWS % RPB == 0, "whole blocks of rows");
   uint32_t off[N];
-  int row_stride;
+  int row_stride, block_stride;
 
-  __device__ __forceinline__ explicit TileLoader(int stride) : row_stride(stride) {
+  __device__ __forceinline__ explicit TileLoader(int stride, int bstride = 0)
+      : row_stride(stride), block_stride(bstride) {
 #pragma unroll
     for (int u = 0; u < N; ++u) {
       const int L = u * NT + threadIdx.x;
       const int r = L / CH;
-      off[u] = 2u * uint32_t(r * stride + 8 * ((L % CH) ^ swz<D>(r)));
+      off[u] = 2u * uint32_t((r % RPB) * stride + (r / RPB) * bstride + 8 * ((L % CH) ^ swz<D>(r)));
     }
   }
 
@@ -286,17 +292,17 @@ struct TileLoader {
   // the same with the tile's LDS byte address
   __device__ __forceinline__ void load_at(uint32_t tile, const u16* g, int nvalid) const {
     const uint32_t lds = tile + 1024u * wave_id();
-    if (nvalid >= ROWS) {  // uniform: a whole tile, the offsets as computed
+    if (nvalid >= RPB) {  // uniform: whole blocks, the offsets as computed
 #pragma unroll
       for (int u = 0; u < N; ++u) lds_copy16(g, off[u], lds + 16u * NT * u);
-    } else {  // the last, ragged tile of a range: a per-lane select, no branch
+    } else {  // the last, ragged rows of a range: a per-lane select, no branch
 #pragma unroll
       for (int u = 0; u < N; ++u) {
         const int L = u * NT + threadIdx.x;
         const int r = L / CH;
-        const uint32_t alt =
-            2u * uint32_t((nvalid - 1) * row_stride + 8 * ((L % CH) ^ swz<D>(r)));
-        lds_copy16(g, r >= nvalid ? alt : off[u], lds + 16u * NT * u);
+        const uint32_t alt = 2u * uint32_t((nvalid - 1) * row_stride + (r / RPB) * block_stride +
+                                           8 * ((L % CH) ^ swz<D>(r)));
+        lds_copy16(g, r % RPB >= nvalid ? alt : off[u], lds + 16u * NT * u);
       }
     }
   }
