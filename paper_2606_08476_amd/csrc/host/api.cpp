@@ -35,11 +35,14 @@ struct FwdWs {
   size_t o_bytes, l_bytes, total;
 };
 // FC_TWO_PASS with received keys: the received partial's fp32 O (the
-// kernel merges it with the local partial in its epilogue)
+// kernel merges it with the local partial in its epilogue), one slot of 32
+// rows x d per wave, four waves per workgroup of the launch
 FwdWs fwd_ws(const View& v, int32_t mode) {
   FwdWs w{};
   if (mode == FC_TWO_PASS && v.t_recv() > 0) {
-    w.o_bytes = align_up(size_t(v.t_q()) * v.hq * v.d * sizeof(float));
+    const size_t wgs = (v.fwd_fused.size() / 8) * size_t(v.hkv) *
+                       size_t(v.hq / v.hkv / v.heads_per_tile);
+    w.o_bytes = align_up(wgs * 4 * 32 * size_t(v.d) * sizeof(float));
     w.total = w.o_bytes;
   }
   return w;

@@ -133,43 +133,51 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   float m = -INFINITY;  // reference row maximum (scaled, log2 units)
   float lsum = 0.f;     // this lane's share of the row sum
 
-  // normalised O and the LSE of the keys seen so far, to o_out/lse_out
-  // (final: bf16 O, plus fp32 O when o_out is non-null)
-  auto write_out = [&](float* o_out, float* lse_out) {
+  // this wave's slot of the merged mode's workspace: 32 x D floats, held in
+  // register order (instruction k of lane l at 256k + 4l), so that the
+  // received partial goes out and comes back with 1 KiB stores and loads
+  // (the lane's address is formed where it is used, from an opaque copy of
+  // the lane index, not held across the loop)
+  auto slot = [&]() {
+    return p.o_f32_recv + (size_t(blockIdx.x) * 4 + wave) * (32 * D) + 4 * opaque(uint32_t(lane));
+  };
+  // paired items: the received partial is complete when the local range
+  // starts; write it (merged: to the slot, with its LSE kept in a register)
+  // and start the local one from empty
+  float lse_recv = -INFINITY;  // merged: the received partial's LSE
+  auto switch_source = [&]() {
     const float tot = sum_halves(lsum);
     const float inv = tot > 0.f ? 1.f / tot : 0.f;
     const float lse = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
-    if (qvalid) {
+    if (MERGED) {
+      lse_recv = lse;
+      if (active) {
+        float* const sl = slot();
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            f32x4 v;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) v[jj] = oacc[db][4 * g + jj] * inv;
+            *reinterpret_cast<f32x4*>(sl + 256 * (4 * db + g)) = v;
+          }
+      }
+    } else if (qvalid) {
+      // (paired partial passes: the caller's [T_q, Hq, D] tensor, stored
+      // from the registers; this is not the benchmarked path)
       const size_t ob = ((size_t)qrow * p.hq + h) * D;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int dcol = 32 * db + 8 * g + 4 * half;
           f32x4 v;
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) v[jj] = oacc[db][4 * g + jj] * inv;
-          if (FINAL) {
-            uint2 packed;
-            packed.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
-            packed.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
-            *reinterpret_cast<uint2*>(p.o_bf16 + ob + dcol) = packed;
-          }
-          if (!FINAL || o_out) *reinterpret_cast<f32x4*>(o_out + ob + dcol) = v;
+          *reinterpret_cast<f32x4*>(p.o_f32_recv + ob + 32 * db + 8 * g + 4 * half) = v;
         }
-      }
-      if (half == 0 && lse_out) lse_out[(size_t)h * p.t_q + qrow] = lse;
+      if (half == 0) p.lse_recv[(size_t)h * p.t_q + qrow] = lse;
     }
-  };
-  // paired items: the received partial is complete when the local range
-  // starts; write it and start the local one from empty
-  float lse_recv = -INFINITY;  // merged: the received partial's LSE
-  auto switch_source = [&]() {
-    if (MERGED) {
-      const float tot = sum_halves(lsum);
-      lse_recv = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
-    }
-    write_out(p.o_f32_recv, MERGED ? nullptr : p.lse_recv);
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = zero16();
     m = -INFINITY;
@@ -332,45 +340,47 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   }
 
   if (PAIRED && n_r == n_t) switch_source();  // no local tile (never empty in practice)
+  // the local (or only) partial, normalised, and its LSE
+  const float tot = sum_halves(lsum);
+  const float inv = tot > 0.f ? 1.f / tot : 0.f;
+  const float lse_own = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
+  // rows go out through the LDS tile buffers, free once the loop's last
+  // barrier has passed: wave w's region is bytes 32*D*4*w ..
+  char* const region = smem + size_t(wave) * (32 * D * 4);
+  const int h0 = kvh * p.group + hc * HPW;
   if constexpr (MERGED) {
-    // local partial (registers) merged with the received one (workspace,
-    // written by this lane at the switch; the waits since have completed it)
+    // local partial (registers) merged with the received one (this wave's
+    // slot, written at the switch; the waits since have completed it)
     wait_async();
-    const float tot = sum_halves(lsum);
-    const float inv = tot > 0.f ? 1.f / tot : 0.f;
-    const float lse_loc = tot > 0.f ? (m + __log2f(tot)) * kLn2 : -INFINITY;
-    const Merge2 w = merge2(lse_loc, lse_recv);
-    if (qvalid) {
-      const size_t ob = ((size_t)qrow * p.hq + h) * D;
-      // every read of the received partial is issued before the first store
-      // (the compiler cannot tell the buffers apart and would otherwise wait
-      // for each read in turn)
-      f32x4 y[DB][4];
+    const Merge2 w = merge2(lse_own, lse_recv);
+    // every read of the received partial is issued before the first use
+    f32x4 y[DB][4];
+    const float* const sl = slot();
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
-          y[db][g] = *reinterpret_cast<const f32x4*>(p.o_f32_recv + ob + 32 * db + 8 * g + 4 * half);
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int dcol = 32 * db + 8 * g + 4 * half;
+      for (int g = 0; g < 4; ++g) y[db][g] = *reinterpret_cast<const f32x4*>(sl + 256 * (4 * db + g));
+    store_rows<D, RPW>(
+        region, active,
+        [&](int db, int g) {
           f32x4 v;
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj)
-            v[jj] = merge2_value(w, oacc[db][4 * g + jj] * inv, y[db][g][jj]);
-          uint2 packed;
-          packed.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
-          packed.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
-          *reinterpret_cast<uint2*>(p.o_bf16 + ob + dcol) = packed;
-          if (p.o_f32) *reinterpret_cast<f32x4*>(p.o_f32 + ob + dcol) = v;
-        }
-      }
-      if (half == 0) p.lse[(size_t)h * p.t_q + qrow] = w.lse;
-    }
+          for (int jj = 0; jj < 4; ++jj) v[jj] = merge2_value(w, oacc[db][4 * g + jj] * inv, y[db][g][jj]);
+          return v;
+        },
+        q0 + wave * RPW, q1, p.hq, h0, p.o_f32, p.o_bf16);
+    if (qvalid && half == 0) p.lse[(size_t)h * p.t_q + qrow] = w.lse;
   } else {
-    write_out(p.o_f32, p.lse);
+    store_rows<D, RPW>(
+        region, active,
+        [&](int db, int g) {
+          f32x4 v;
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) v[jj] = oacc[db][4 * g + jj] * inv;
+          return v;
+        },
+        q0 + wave * RPW, q1, p.hq, h0, p.o_f32, FINAL ? p.o_bf16 : nullptr);
+    if (qvalid && half == 0) p.lse[(size_t)h * p.t_q + qrow] = lse_own;
   }
 }
 

@@ -210,18 +210,17 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
     if (j + 1 < n_t) step(j + 1, std::integral_constant<int, 1>());
   }
 
-  if (qvalid) {
-    float* out = p.dq + ((size_t)qrow * p.hq + h) * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
+  // dQ rows out through this wave's share of the (now free) K/V buffers,
+  // 1 KiB per store instruction
+  store_rows<D, RPW>(
+      smem + size_t(wave) * (32 * D * 4), active,
+      [&](int db, int g) {
         f32x4 v;
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) v[jj] = p.scale * dq[db][4 * g + jj];
-        *reinterpret_cast<f32x4*>(out + 32 * db + 8 * g + 4 * half) = v;
-      }
-  }
+        return v;
+      },
+      q0 + wave * RPW, q1, p.hq, kvh * p.group + hc * HPW, p.dq, nullptr);
 }
 
 }  // namespace fck

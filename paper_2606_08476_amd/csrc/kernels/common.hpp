@@ -308,6 +308,74 @@ struct TileLoader {
   }
 };
 
+// Coalesced store of one wave's 32 output rows (query row, head) of D
+// values. Lane l holds, for pair p = l % 32, columns 32db + 8g + 4(l/32) +
+// 0..3 in val(db, g) (the MFMA accumulator layout of O^T or dQ^T); pair p
+// is row row0 + p % RPW of head h0 + p / RPW of a [rows, hq, D] tensor, so the
+// heads of a row lie side by side in memory. Stored straight from
+// the registers, every store instruction would scatter over 32 rows; here
+// the wave first writes its rows to its own LDS region (32 x D floats, 16-byte
+// chunks XOR-swizzled by row) and then stores them so that each instruction
+// covers 1 KiB of consecutive addresses (fp32), or 1 KiB of bf16. Rows at or
+// past row_end are not stored; out_f32 or out_bf16 may be null. Every wave
+// of the workgroup must call it (it holds a barrier); `active` false skips
+// the wave's stores, and the LDS regions must be free of other use.
+template <int D, int RPW, class Val>
+__device__ __forceinline__ void store_rows(char* region, bool active, Val val, int row0,
+                                           int row_end, int hq, int h0, float* out_f32,
+                                           u16* out_bf16) {
+  constexpr int CH = D / 4;           // 16-byte chunks per row
+  constexpr int U = (32 / RPW) * D;   // values per row0 + r: its heads side by side
+  const int lane = threadIdx.x & 63, p = lane & 31, half = lane >> 5;
+  float* st = reinterpret_cast<float*>(region);
+  if (active) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = 8 * db + 2 * g + half;
+        *reinterpret_cast<f32x4*>(st + p * D + 4 * (c ^ (p % CH))) = val(db, g);
+      }
+  }
+  __syncthreads();
+  if (!active) return;
+  // value e of the wave's output, in memory order: row row0 + e / U, head
+  // h0 + (e % U) / D, column e % D
+  auto at = [&](int e, int& pr, int& row, size_t& gofs) {
+    const int r = e / U, u = e % U, hoff = u / D, dd = u % D;
+    pr = hoff * RPW + r;
+    row = row0 + r;
+    gofs = (size_t(row) * hq + h0 + hoff) * D + dd;
+    return dd;
+  };
+  if (out_f32) {
+#pragma unroll
+    for (int s = 0; s < D / 8; ++s) {
+      int pr, row;
+      size_t go;
+      const int dd = at(256 * s + 4 * lane, pr, row, go);
+      const f32x4 v = *reinterpret_cast<const f32x4*>(st + pr * D + 4 * ((dd / 4) ^ (pr % CH)));
+      if (row < row_end) *reinterpret_cast<f32x4*>(out_f32 + go) = v;
+    }
+  }
+  if (out_bf16) {
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+      int pr, row;
+      size_t go;
+      const int dd = at(512 * s + 8 * lane, pr, row, go);
+      const f32x4 a = *reinterpret_cast<const f32x4*>(st + pr * D + 4 * ((dd / 4) ^ (pr % CH)));
+      const f32x4 b = *reinterpret_cast<const f32x4*>(st + pr * D + 4 * ((dd / 4 + 1) ^ (pr % CH)));
+      uint4 pk;
+      pk.x = uint32_t(f2bf(a[0])) | (uint32_t(f2bf(a[1])) << 16);
+      pk.y = uint32_t(f2bf(a[2])) | (uint32_t(f2bf(a[3])) << 16);
+      pk.z = uint32_t(f2bf(b[0])) | (uint32_t(f2bf(b[1])) << 16);
+      pk.w = uint32_t(f2bf(b[2])) | (uint32_t(f2bf(b[3])) << 16);
+      if (row < row_end) *reinterpret_cast<uint4*>(out_bf16 + go) = pk;
+    }
+  }
+}
+
 // Log-sum-exp merge of two partial results over disjoint key sets (weights
 // of the partials and the merged LSE, natural log; a -inf partial has
 // weight 0, so two empty partials merge to O = 0, LSE = -inf). One

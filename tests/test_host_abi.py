@@ -215,8 +215,11 @@ def test_kernel_calls_rejected_before_launch():
     assert lib.fc_lse_merge(1, 1, 1, 1, -1, 2, 64, 1, None, 1, None) == -1
     f, b, k = v.workspace_size(F.FC_TWO_PASS)
     i = v.info
-    # the two-pass forward keeps the received partial's fp32 O (merged in the kernel)
-    assert f == (i["t_q"] * 4 * 64 * 4 + 255) // 256 * 256
+    # the two-pass forward keeps the received partial's fp32 O (merged in the
+    # kernel): a slot of 32 rows x d per wave, 4 waves per workgroup of the
+    # launch (fused items x KV heads x head chunks)
+    wgs = i["n_fwd_fused"] * i["hkv"] * (i["hq"] // i["hkv"] // (128 // i["bm_fwd"]))
+    assert f == (wgs * 4 * 32 * i["d"] * 4 + 255) // 256 * 256
     assert v.workspace_size(F.FC_FUSED)[0] == 0
     assert lib.fc_workspace_size(h, 7, None, None, None) == -1
     assert k == 0 and b == ((i["t_q"] * 4 * 4 + 255) // 256) * 256   # no split key tile here
