@@ -89,18 +89,16 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   const int kw = k0 + 32 * wave;
   const int qfirst = p.qfirst[4 * item + wave];
 
-  // key tile (rows past k1 repeat the last key; they are masked)
-  TileLoader<D, BN>(p.hkv * D).load_at(lds_addr(smem) + OK, Kg + size_t(k0) * kvs + kvo, k1 - k0);
-  const int kidx = k0 + 32 * wave + (lane & 31);  // this lane's key
-  const bool kvalid = kidx < k1;
+  // key tile, and the same rows of V over the Q/dO buffers (read into
+  // registers before the first Q/dO copy); rows past k1 repeat the last
+  // key, whose P is masked to 0
+  {
+    const TileLoader<D, BN> ldk(p.hkv * D);
+    ldk.load_at(lds_addr(smem) + OK, Kg + size_t(k0) * kvs + kvo, k1 - k0);
+    ldk.load_at(lds_addr(smem) + OQ0, Vg + size_t(k0) * kvs + kvo, k1 - k0);
+  }
   // V rows of this lane's key as the B operand of dP = dO V^T
   bf16x8 vreg[KS];
-  {
-    const u16* vp = Vg + size_t(kidx) * kvs + kvo + 8 * half;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      vreg[ks] = kvalid ? *reinterpret_cast<const bf16x8*>(vp + 16 * ks) : zero8();
-  }
 
   const int ntile = (q1 - q0 + RPI - 1) / RPI;
   const int n_it = ntile * (p.group / HPI);
@@ -158,6 +156,14 @@ __device__ __forceinline__ void dkdv_tile(const BwdParams& p, int b, char* smem)
   const bool kfull = k1 - k0 == BN;
   const float sl2 = p.scale * kLog2e;
 
+  wait_async();
+  __syncthreads();
+  {
+    const int vb = row_base<D>(32 * wave, lane);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) vreg[ks] = lds_b128(smem, 2u * uint32_t(vb ^ (ks << 4)), OQ0);
+  }
+  __syncthreads();  // every wave holds its V rows before the Q/dO copies
   if (n_it > 0) fetch(0, 0, 0);
   advance();
   wait_async();

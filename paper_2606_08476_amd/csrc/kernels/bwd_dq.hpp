@@ -71,21 +71,17 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
     ld.load_at(lds_addr(smem) + kofs + TILE, (rs ? p.v_recv : p.v_loc) + base, hi - k0);
   };
 
-  if (n_t > 0) fetch(0, 0);
+  // the workgroup's Q and dO rows through LDS first (Q over the second K/V
+  // buffer, dO over the first), then key tile 0
+  const int h0 = kvh * p.group + hc * HPW;
+  load_pairs<D, RPW>(lds_addr(smem) + 2 * TILE, p.q, q0, q1, p.hq, h0);
+  load_pairs<D, RPW>(lds_addr(smem), p.dout, q0, q1, p.hq, h0);
 
   bf16x8 qreg[KS], oreg[KS];
   float lse2 = 0.f, del = 0.f;
-  {
-    const size_t rb = ((size_t)qrow * p.hq + h) * D + 8 * half;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      qreg[ks] = qvalid ? *reinterpret_cast<const bf16x8*>(p.q + rb + 16 * ks) : zero8();
-      oreg[ks] = qvalid ? *reinterpret_cast<const bf16x8*>(p.dout + rb + 16 * ks) : zero8();
-    }
-    if (qvalid) {
-      lse2 = p.lse[(size_t)h * p.t_q + qrow] * kLog2e;
-      del = p.delta[(size_t)h * p.t_q + qrow];
-    }
+  if (qvalid) {
+    lse2 = p.lse[(size_t)h * p.t_q + qrow] * kLog2e;
+    del = p.delta[(size_t)h * p.t_q + qrow];
   }
 
   // per-lane LDS byte offsets: K/V rows for k-step ks, and the two transpose
@@ -105,6 +101,18 @@ __device__ __forceinline__ void dq_tile(const DqParams& p, int b, char* smem) {
   f32x16 dq[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
+  wait_async();
+  __syncthreads();
+  if (active) {
+    const int qb = row_base<D>(32 * wave, lane);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qreg[ks] = lds_b128(smem, 2u * uint32_t(qb ^ (ks << 4)), 2 * TILE);
+      oreg[ks] = lds_b128(smem, 2u * uint32_t(qb ^ (ks << 4)), 0);
+    }
+  }
+  __syncthreads();  // every wave holds its rows before tile 0 overwrites them
+  if (n_t > 0) fetch(0, 0);
   wait_async();
   __syncthreads();
 

@@ -308,6 +308,33 @@ struct TileLoader {
   }
 };
 
+// Asynchronous copy of a workgroup's 128 (query row, head) rows of D bf16
+// from a [rows, hq, D] tensor into a swizzled 128 x D LDS tile, whose row
+// 32w + p is pair p of wave w: row row0 + RPW*w + p % RPW, head h0 + p / RPW
+// (the lane-to-pair map of the forward and dQ workgroups). Each wave then
+// reads its 32 rows as an MFMA operand with row reads (row_base(32w, lane)).
+// Loaded lane by lane from registers, these rows cost one scattered 16-byte
+// piece per row and instruction; copied this way every instruction moves
+// 1 KiB in whole 16-byte chunks. Rows at or past row_end repeat row
+// row_end - 1 (finite data for lanes without a row).
+template <int D, int RPW>
+__device__ __forceinline__ void load_pairs(uint32_t tile, const u16* g, int row0, int row_end,
+                                           int hq, int h0) {
+  constexpr int CH = D / 8;
+  constexpr int N = 128 * CH / 256;
+  const u16* base = g + (size_t(row0) * hq + h0) * D;
+  const uint32_t lds = tile + 1024u * wave_id();
+  const int last = row_end - 1 - row0;
+#pragma unroll
+  for (int u = 0; u < N; ++u) {
+    const int L = u * 256 + int(threadIdx.x);
+    const int R = L / CH, w = R / 32, pr = R % 32;
+    const int rr = min(RPW * w + pr % RPW, last);
+    const uint32_t off = 2u * uint32_t((rr * hq + pr / RPW) * D + 8 * ((L % CH) ^ swz<D>(R)));
+    lds_copy16(base, off, lds + 16u * 256 * u);
+  }
+}
+
 // Coalesced store of one wave's 32 output rows (query row, head) of D
 // values. Lane l holds, for pair p = l % 32, columns 32db + 8g + 4(l/32) +
 // 0..3 in val(db, g) (the MFMA accumulator layout of O^T or dQ^T); pair p
