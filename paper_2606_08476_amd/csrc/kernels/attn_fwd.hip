@@ -7,10 +7,10 @@
 // one KV head. Each wave owns 32/heads_per_tile query rows of every one of
 // those heads (a query per lane). Key tiles of 64 keys are double-buffered
 // in LDS and shared by the waves (and so by the heads of the group); later
-// tiles are copied from HBM straight into LDS
-// (asynchronous loads, no staging registers) while the current one is
-// computed, and the loop is software-pipelined across tiles (the scores of
-// the next tile are computed beside the softmax of the current one):
+// tiles are copied from HBM straight into LDS (asynchronous loads, no
+// staging registers) while the current one is computed, and the loop is
+// software-pipelined across tiles (the scores of the next tile are computed
+// beside the softmax of the current one):
 //   S^T = K Q^T        MFMA 32x32x16, Q held in registers (B operand), so a
 //                      query is a lane and its row statistics are per lane;
 //   online softmax     base 2, scale folded into one FMA per score; a row's

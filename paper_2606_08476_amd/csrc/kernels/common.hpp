@@ -313,7 +313,7 @@ struct TileLoader {
 // 32w + p is pair p of wave w: row row0 + RPW*w + p % RPW, head h0 + p / RPW
 // (the lane-to-pair map of the forward and dQ workgroups). Each wave then
 // reads its 32 rows as an MFMA operand with row reads (row_base(32w, lane)).
-// Loaded lane by lane from registers, these rows cost one scattered 16-byte
+// Loaded lane by lane into registers, these rows cost one scattered 16-byte
 // piece per row and instruction; copied this way every instruction moves
 // 1 KiB in whole 16-byte chunks. Rows at or past row_end repeat row
 // row_end - 1 (finite data for lanes without a row).
@@ -338,15 +338,16 @@ __device__ __forceinline__ void load_pairs(uint32_t tile, const u16* g, int row0
 // Coalesced store of one wave's 32 output rows (query row, head) of D
 // values. Lane l holds, for pair p = l % 32, columns 32db + 8g + 4(l/32) +
 // 0..3 in val(db, g) (the MFMA accumulator layout of O^T or dQ^T); pair p
-// is row row0 + p % RPW of head h0 + p / RPW of a [rows, hq, D] tensor, so the
-// heads of a row lie side by side in memory. Stored straight from
-// the registers, every store instruction would scatter over 32 rows; here
-// the wave first writes its rows to its own LDS region (32 x D floats, 16-byte
-// chunks XOR-swizzled by row) and then stores them so that each instruction
-// covers 1 KiB of consecutive addresses (fp32), or 1 KiB of bf16. Rows at or
-// past row_end are not stored; out_f32 or out_bf16 may be null. Every wave
-// of the workgroup must call it (it holds a barrier); `active` false skips
-// the wave's stores, and the LDS regions must be free of other use.
+// is row row0 + p % RPW of head h0 + p / RPW of a [rows, hq, D] tensor, so
+// the heads of a row lie side by side in memory. Stored straight from the
+// registers, every store instruction would scatter over 32 rows; here the
+// wave first writes its rows to its own LDS region (32 x D floats, 16-byte
+// chunks XOR-swizzled by row) and then stores them so that each
+// instruction covers 1 KiB of consecutive addresses (fp32), or 1 KiB of
+// bf16. Rows at or past row_end are not stored; out_f32 or out_bf16 may be
+// null. Every wave of the workgroup must call it (it contains a barrier);
+// `active` false skips the wave's stores, and the LDS regions must be free
+// of other use.
 template <int D, int RPW, class Val>
 __device__ __forceinline__ void store_rows(char* region, bool active, Val val, int row0,
                                            int row_end, int hq, int h0, float* out_f32,
