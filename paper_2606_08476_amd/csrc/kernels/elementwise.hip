@@ -108,7 +108,8 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const void* __restrict__ o
 }
 
 // Sum of the partial dK/dV of a split key tile, in slot order. One
-// workgroup per (split tile, KV head); entries are (src, k0, k1, first slot,
+// workgroup per (split tile, KV head, 16 of the tile's 128 keys), so that a
+// few split tiles still fill the chip; entries are (src, k0, k1, first slot,
 // slot count, 0, 0, 0); partial slots hold 128 rows of d values per KV head.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(const int32_t* __restrict__ entries,
@@ -116,19 +117,39 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const int32_t* __restri
                                                          const float* __restrict__ pv, int32_t hkv,
                                                          float* dk_loc, float* dv_loc,
                                                          float* dk_recv, float* dv_recv) {
-  constexpr int BN = 128, C4 = D / 4;
-  const int kvh = blockIdx.x % hkv;
-  const int32_t* e = entries + 8 * (blockIdx.x / hkv);
+  constexpr int BN = 128, C4 = D / 4, ROWS = 16;  // rows of the key tile per workgroup
+  constexpr int PER = ROWS * C4 / 256;            // 16-byte chunks per thread
+  const int rb = blockIdx.x % (BN / ROWS);
+  const int kvh = (blockIdx.x / (BN / ROWS)) % hkv;
+  const int32_t* e = entries + 8 * (blockIdx.x / (BN / ROWS) / hkv);
   const int src = e[0], k0 = e[1], k1 = e[2], s0 = e[3], ns = e[4];
   float* dk = src ? dk_recv : dk_loc;
   float* dv = src ? dv_recv : dv_loc;
-  for (int idx = threadIdx.x; idx < (k1 - k0) * C4; idx += 256) {
-    const int r = idx / C4, c = idx % C4;
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int idx = u * 256 + int(threadIdx.x);
+    const int r = rb * ROWS + idx / C4, c = idx % C4;
+    if (k0 + r >= k1) continue;
+    // the slots in their fixed order, two loads of each in flight at once
     f32x4 ak = {0.f, 0.f, 0.f, 0.f}, av = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < ns; ++s) {
-      const size_t o = ((size_t(s0 + s) * hkv + kvh) * BN + r) * D;
-      const f32x4 x = reinterpret_cast<const f32x4*>(pk + o)[c];
-      const f32x4 y = reinterpret_cast<const f32x4*>(pv + o)[c];
+    auto at = [&](int s) { return ((size_t(s0 + s) * hkv + kvh) * BN + r) * D; };
+    int s = 0;
+    for (; s + 1 < ns; s += 2) {
+      const f32x4 x0 = reinterpret_cast<const f32x4*>(pk + at(s))[c];
+      const f32x4 y0 = reinterpret_cast<const f32x4*>(pv + at(s))[c];
+      const f32x4 x1 = reinterpret_cast<const f32x4*>(pk + at(s + 1))[c];
+      const f32x4 y1 = reinterpret_cast<const f32x4*>(pv + at(s + 1))[c];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        ak[j] += x0[j];
+        ak[j] += x1[j];
+        av[j] += y0[j];
+        av[j] += y1[j];
+      }
+    }
+    if (s < ns) {
+      const f32x4 x = reinterpret_cast<const f32x4*>(pk + at(s))[c];
+      const f32x4 y = reinterpret_cast<const f32x4*>(pv + at(s))[c];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         ak[j] += x[j];
@@ -191,7 +212,7 @@ hipError_t launch_bwd_reduce(const int32_t* entries, int32_t n, const float* par
                              const float* part_v, int32_t hkv, int32_t d, float* dk_loc,
                              float* dv_loc, float* dk_recv, float* dv_recv, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  const dim3 grid(unsigned(n) * hkv), block(256);
+  const dim3 grid(unsigned(n) * hkv * 8), block(256);  // 8 row blocks of 16 keys per tile
   if (d == 64)
     hipLaunchKernelGGL(bwd_reduce_kernel<64>, grid, block, 0, s, entries, part_k, part_v, hkv,
                        dk_loc, dv_loc, dk_recv, dv_recv);
