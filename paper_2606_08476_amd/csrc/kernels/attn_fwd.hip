@@ -355,11 +355,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     const Merge2 w = merge2(lse_own, lse_recv);
     // every read of the received partial is issued before the first use
     f32x4 y[DB][4];
-    const float* const sl = slot();
+    if (active) {  // (a wave without rows wrote no slot)
+      const float* const sl = slot();
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) y[db][g] = *reinterpret_cast<const f32x4*>(sl + 256 * (4 * db + g));
+        for (int g = 0; g < 4; ++g)
+          y[db][g] = *reinterpret_cast<const f32x4*>(sl + 256 * (4 * db + g));
+    }
     store_rows<D, RPW>(
         region, active,
         [&](int db, int g) {
