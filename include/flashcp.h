@@ -161,11 +161,13 @@ typedef struct {
 /* Tile shapes of a view; 0 in a field selects its default.
  *   bm_fwd  query rows per workgroup of the forward and of the dQ pass: 32,
  *           64 or 128, i.e. 4, 2 or 1 query heads of a KV-head group per
- *           workgroup (each wave takes 32 rows of one head); 128/bm_fwd must
- *           divide Hq/Hkv. Default: as many heads per workgroup as the group
+ *           workgroup (each wave takes a quarter of the rows of every one of
+ *           those heads, a (row, head) per lane); 128/bm_fwd must divide
+ *           Hq/Hkv. Default: as many heads per workgroup as the group
  *           allows, min(Hq/Hkv, 4) (bm_fwd = 32 when Hq/Hkv >= 4).
  *   bn_fwd  keys per forward / dQ tile: 64 (the compiled shape).
- *   bm_bwd  query rows per dK/dV iteration: 32 (compiled).
+ *   bm_bwd  (query row, head) pairs per dK/dV iteration: 32 (compiled;
+ *           8 rows of 4 heads, 16 of 2 or 32 of 1, as the group allows).
  *   bn_bwd  keys per dK/dV workgroup: 128 (compiled).
  * Other values give FC_ERR_UNSUPPORTED. */
 typedef struct {
