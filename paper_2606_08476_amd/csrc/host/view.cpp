@@ -276,8 +276,9 @@ int build_view(const int32_t* cu, int32_t n_docs, const fc_shard* shards, int64_
   v.hq = hq;
   v.hkv = hkv;
   v.d = d;
-  // tile shapes: the forward / dQ query tile is 32 rows per wave times the
-  // waves per head, 4 / (heads per workgroup); the other shapes are compiled
+  // tile shapes: the forward / dQ query tile is 128 / (heads per workgroup)
+  // rows, each of the 4 waves taking a quarter of them for every head; the
+  // other shapes are compiled
   const fc_tile_cfg t = tiles ? *tiles : fc_tile_cfg{0, 0, 0, 0};
   if (t.bm_fwd == 0) {
     v.heads_per_tile = std::min(G, 4);
