@@ -359,3 +359,42 @@ def test_repeat_runs_deterministic(dev):
     b = Run(_cases.small_case("longdoc_16k"), dev)
     for n in ("o", "lse", "dq", "dk_loc", "dv_loc", "dk_recv", "dv_recv"):
         assert torch.equal(getattr(a, n), getattr(b, n)), n
+
+
+def test_empty_rank_calls_are_noops(dev):
+    """A rank the plan gives no token (ten tokens, both shards on rank 0 of
+    two) has an empty view: every entry point accepts its zero-row tensors,
+    launches nothing and returns success, and the stream stays usable."""
+    cu = np.array([0, 10], dtype=np.int32)
+    plan = np.array([[0, 0, 0, 10]], dtype=np.int32)
+    hq, hkv, d = 8, 2, 128
+    v = F.View(cu, plan, 2, 1, hq, hkv, d).bind(dev)
+    i = v.info
+    assert i["t_q"] == 0 and i["t_recv"] == 0
+    bf, f32 = torch.bfloat16, torch.float32
+    e = lambda *s, dt=bf: torch.empty(*s, dtype=dt, device=dev)
+    q, do = e(0, hq, d), e(0, hq, d)
+    kl, vl, kr, vr = e(0, hkv, d), e(0, hkv, d), e(0, hkv, d), e(0, hkv, d)
+    kp = torch.randn(10, hkv, d, device=dev).to(bf)
+    vp = torch.randn(10, hkv, d, device=dev).to(bf)
+    o, o32, lse = e(0, hq, d), e(0, hq, d, dt=f32), e(hq, 0, dt=f32)
+    delta, dq = e(hq, 0, dt=f32), e(0, hq, d, dt=f32)
+    dkl, dvl, dkr, dvr = (e(0, hkv, d, dt=f32) for _ in range(4))
+    fws, _, bws = v.workspace_size(F.FC_TWO_PASS)
+    ws = torch.empty(max(fws, bws, 1), dtype=torch.uint8, device=dev)
+    F.fc_kv_gather(v, kp, vp, kl, vl, kr, vr)
+    for mode in (F.FC_TWO_PASS, F.FC_FUSED):
+        F.fc_attn_fwd(v, q, kl, vl, kr, vr, 0.0, mode, o, o32, lse, ws)
+    F.fc_attn_fwd_partials(v, q, kl, vl, kr, vr, 0.0, o32, lse, e(0, hq, d, dt=f32), e(hq, 0, dt=f32))
+    F.fc_bwd_preprocess(v, o, do, delta, o_f32=o32)
+    for det in (True, False):
+        F.fc_attn_bwd(v, q, kl, vl, kr, vr, o, lse, do, 0.0, dq, dkl, dvl, dkr, dvr, ws,
+                      deterministic=det, o_f32=o32)
+        F.fc_attn_bwd_pass(v, q, kl, vl, kr, vr, lse, delta, do, 0.0, dq, dkl, dvl, dkr, dvr,
+                           ws, deterministic=det)
+        F.fc_attn_bwd_noalloc(v, q, kl, vl, kr, vr, o, lse, do, 0.0, dq, dkl, dvl, dkr, dvr,
+                              deterministic=det, o_f32=o32)
+    torch.cuda.synchronize()
+    # the stream still runs work after the no-op calls
+    assert float((kp.float() * 2).sum().item()) == pytest.approx(float(kp.float().sum().item()) * 2, rel=1e-5)
+    v.close()
