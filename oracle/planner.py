@@ -27,8 +27,9 @@ notes):
   most tokens above C/N (lowest index on ties); pop its whole-document
   pieces last-in-first-out until the popped tokens cover the excess e; the
   worker keeps the tail of the last popped piece so it ends at exactly C/N,
-  and gives away that piece's head plus every earlier popped piece. Each
-  given piece is handed out in document order to under-full workers, the
+  and gives away that piece's head plus every earlier popped piece. The
+  given pieces are handed out in the order they were popped (the head
+  last), each from its first token on, to under-full workers, the
   least-loaded (W, then index) first, each taking as many tokens as it has
   room for. Only document prefixes move, matching Sec. 3.3 (only the lower
   segments are exchanged; cost proportional to the moved length).
@@ -40,10 +41,11 @@ notes):
   in that order. The loop ends when Cur_R <= R or every document is Per-Doc.
 
 Parity: pinned by closed forms (W, Per-Doc pairs c(2Nc+1)), the
-constraints Eq. 1 and Eq. 2, a hand-checked LPT input, and brute force over
-all whole-document placements for N = 2 (see tests/test_oracle_planner.py).
-The hybrid's exact shard boundaries follow the reading above and are
-otherwise parity unpinned beyond those invariants.
+constraints Eq. 1 and Eq. 2, a hand-checked LPT input, brute force over
+all whole-document placements for N = 2, and three hybrid inputs worked by
+hand under the reading above (two and three workers, up to three passes, a
+repair that pops two pieces and splits a given piece over two receivers;
+tests/golden/planner_hand.json, tests/test_oracle_planner.py).
 """
 from __future__ import annotations
 

@@ -6,9 +6,10 @@
 //   the worker with the largest token excess e (lowest index on ties) pops its
 //   whole-document pieces last-in-first-out until they cover e, keeps the
 //   tail of the last popped piece so that it ends at exactly C/N tokens, and
-//   hands the head of that piece and every earlier popped piece, in document
-//   order, to the under-full workers with the least workload (lowest index on
-//   ties), each taking what it has room for. Only document prefixes move, so
+//   hands every earlier popped piece and then the head of that piece, in the
+//   order they were popped and each from its first token on, to the
+//   under-full workers with the least workload (lowest index on ties), each
+//   taking what it has room for. Only document prefixes move, so
 //   the extra receive volume stays proportional to the moved length (Sec. 3.3).
 #include <algorithm>
 #include <cstring>

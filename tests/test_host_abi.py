@@ -66,6 +66,26 @@ def test_planners_bit_exact_random():
             assert F.fc_plan_stats(cu, N, a, 2, 64) == P.stats(cu, N, b, 2, 64)
 
 
+def test_planners_match_hand_worked_examples():
+    """The library's LPT and hybrid planners and plan statistics on the
+    examples of tests/golden worked by hand from Algorithm 1."""
+    import json
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "planner_hand.json")))
+    g = gold["lpt"]
+    cu = np.concatenate([[0], np.cumsum(g["lengths"])])
+    plan = F.fc_plan_whole_lpt(cu, g["cp"])
+    assert plan.tolist() == g["plan"]
+    assert F.fc_plan_stats(cu, g["cp"], plan, 1, 1)["work"] == g["work"]
+    for g in [gold["hybrid"]] + gold["hybrid_more"]:
+        cu = np.concatenate([[0], np.cumsum(g["lengths"])])
+        plan, isp = F.fc_plan_hybrid(cu, g["cp"], g["target_r"])
+        assert plan.tolist() == g["plan"] and isp.tolist() == g["is_per_doc"]
+        st = F.fc_plan_stats(cu, g["cp"], plan, 1, 1)
+        assert st["work"] == g["work"] and st["tokens"] == g["tokens"]
+        assert st["recv_tokens"] == g["recv_tokens"]
+        assert st["eq4"] == g["eq4_over_hkv_d"] and st["eq5"] == g["eq5_over_hkv_d"]
+
+
 @pytest.mark.parametrize("name", list(synth.WORKLOADS))
 def test_planners_bit_exact_workloads(name):
     w = synth.WORKLOADS[name]

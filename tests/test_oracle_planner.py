@@ -117,8 +117,13 @@ def test_lpt_within_graham_bound_of_brute_force():
     assert _brute_opt(GOLD["lpt"]["lengths"], 2) == GOLD["lpt"]["brute_force_optimum_max_work"]
 
 
-def test_hybrid_hand_example():
-    g = GOLD["hybrid"]
+@pytest.mark.parametrize("i", range(1 + len(GOLD["hybrid_more"])))
+def test_hybrid_hand_example(i):
+    """Algorithm 1 worked by hand: two passes on two workers (the first
+    example), three passes on three workers, and one pass on three workers
+    whose repair pops two pieces and splits a given piece over two
+    receivers."""
+    g = GOLD["hybrid"] if i == 0 else GOLD["hybrid_more"][i - 1]
     cu = _cu(g["lengths"])
     plan, isp = P.plan_hybrid(cu, g["cp"], g["target_r"])
     assert plan.tolist() == g["plan"]
