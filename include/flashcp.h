@@ -26,6 +26,9 @@
  *   - The caller owns every buffer it passes. Device pointers must point to
  *     device memory of at least the size stated; the library cannot check
  *     their extent. Host pointers are read or written before return.
+ *   - Alignment: tensors of d-element rows (q, k, v, o, dout, dq, dk, dv,
+ *     fp32 outputs and partials) and workspaces 16 bytes, lse and delta 4
+ *     bytes; a misaligned pointer is rejected with FC_ERR_INVALID_ARG.
  *   - The library owns fc_view objects (host memory only). A view is bound
  *     to a caller-owned device buffer by fc_view_bind; that buffer must stay
  *     alive and unmodified while work launched with the view is in flight.

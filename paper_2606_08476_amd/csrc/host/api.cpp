@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdint>
+#include <initializer_list>
 
 #include "../kernels/launch.hpp"
 #include "internal.hpp"
@@ -21,6 +23,20 @@ int check_view(fc_view view, View*& v) {
   if (!view) return fail(FC_ERR_INVALID_ARG, "view is null");
   v = reinterpret_cast<View*>(view);
   if (!v->dev_meta) return fail(FC_ERR_WORKSPACE, "view is not bound to device metadata");
+  return FC_OK;
+}
+
+// The kernels move tensor rows with 16-byte vector accesses and read
+// LSE/delta per element: row tensors and workspaces must be 16-byte aligned,
+// LSE and delta 4-byte aligned (NULL pointers are checked elsewhere).
+int check_aligned(std::initializer_list<const void*> rows,
+                  std::initializer_list<const void*> scalars = {}) {
+  for (const void* p : rows)
+    if (reinterpret_cast<uintptr_t>(p) % 16)
+      return fail(FC_ERR_INVALID_ARG, "tensor and workspace pointers must be 16-byte aligned");
+  for (const void* p : scalars)
+    if (reinterpret_cast<uintptr_t>(p) % 4)
+      return fail(FC_ERR_INVALID_ARG, "lse and delta pointers must be 4-byte aligned");
   return FC_OK;
 }
 
@@ -199,6 +215,7 @@ int fc_workspace_size(fc_view view, int32_t mode, size_t* fwd_bytes, size_t* bwd
 int fc_kv_gather(fc_view view, const void* k_packed, const void* v_packed, int64_t t_packed,
                  void* k_loc, void* v_loc, void* k_recv, void* v_recv, void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({k_packed, v_packed, k_loc, v_loc, k_recv, v_recv})) return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() + v->t_recv() == 0) return FC_OK;
@@ -230,6 +247,7 @@ int fc_attn_fwd_partial(fc_view view, int32_t src, const void* q, const void* k_
                         const void* v_src, float scale, float* o_part, float* lse_part,
                         void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({q, k_src, v_src, o_part}, {lse_part})) return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (src != 0 && src != 1) return fail(FC_ERR_INVALID_ARG, "src must be 0 or 1");
@@ -256,6 +274,9 @@ int fc_attn_fwd_partials(fc_view view, const void* q, const void* k_loc, const v
                          const void* k_recv, const void* v_recv, float scale, float* o_loc,
                          float* lse_loc, float* o_recv, float* lse_recv, void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({q, k_loc, v_loc, k_recv, v_recv, o_loc, o_recv},
+                              {lse_loc, lse_recv}))
+    return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
@@ -270,6 +291,7 @@ int fc_attn_fwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
                 const void* k_recv, const void* v_recv, float scale, int32_t mode, void* o,
                 float* o_f32, float* lse, void* ws, size_t ws_bytes, void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({q, k_loc, v_loc, k_recv, v_recv, o, o_f32, ws}, {lse})) return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (mode != FC_TWO_PASS && mode != FC_FUSED) return fail(FC_ERR_INVALID_ARG, "bad mode");
@@ -313,6 +335,7 @@ int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const f
                  int32_t t, int32_t h, int32_t d, void* o_bf16, float* o_f32, float* lse_out,
                  void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({o_a, o_b, o_bf16, o_f32}, {lse_a, lse_b, lse_out})) return rc;
   if (t < 0 || h < 0) return fail(FC_ERR_INVALID_ARG, "negative size");
   if (d != 64 && d != 128) return fail(FC_ERR_UNSUPPORTED, "head dim must be 64 or 128");
   if (int64_t(t) * h == 0) return FC_OK;
@@ -327,12 +350,11 @@ int fc_lse_merge(const float* o_a, const float* lse_a, const float* o_b, const f
 int fc_bwd_preprocess(fc_view view, const void* o, const float* o_f32, const void* dout,
                       float* delta, void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({o, o_f32, dout}, {delta})) return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
   if ((!o && !o_f32) || !dout || !delta) return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  if (o_f32 && reinterpret_cast<uintptr_t>(o_f32) % 16)
-    return fail(FC_ERR_INVALID_ARG, "o_f32 must be 16-byte aligned");
   return hip_status(fck::launch_bwd_preprocess(static_cast<const uint16_t*>(o), o_f32,
                                                static_cast<const uint16_t*>(dout), delta,
                                                v->t_q(), v->hq, v->d, nullptr,
@@ -345,6 +367,10 @@ int fc_attn_bwd_dkdv(fc_view view, const void* q, const void* k_loc, const void*
                      const void* dout, float scale, float* dk_loc, float* dv_loc, float* dk_recv,
                      float* dv_recv, void* ws, size_t ws_bytes, void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({q, k_loc, v_loc, k_recv, v_recv, dout, dk_loc, dv_loc, dk_recv,
+                               dv_recv, ws},
+                              {lse, delta}))
+    return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
@@ -366,6 +392,7 @@ int fc_attn_bwd_dq(fc_view view, const void* q, const void* k_loc, const void* v
                    const void* k_recv, const void* v_recv, const float* lse, const float* delta,
                    const void* dout, float scale, float* dq, void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({q, k_loc, v_loc, k_recv, v_recv, dout, dq}, {lse, delta})) return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
@@ -384,13 +411,16 @@ int fc_attn_bwd_pass(fc_view view, const void* q, const void* k_loc, const void*
                      float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv, void* ws,
                      size_t ws_bytes, void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({q, k_loc, v_loc, k_recv, v_recv, dout, dq, dk_loc, dv_loc, dk_recv,
+                               dv_recv, ws},
+                              {lse, delta}))
+    return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
   if (!q || !k_loc || !v_loc || !lse || !delta || !dout || !dq || !dk_loc || !dv_loc ||
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  if (reinterpret_cast<uintptr_t>(dq) % 16) return fail(FC_ERR_INVALID_ARG, "dq must be 16-byte aligned");
   const size_t need = part_ws(*v);
   if (need && (!ws || ws_bytes < need))
     return fail(FC_ERR_WORKSPACE, "dK/dV workspace of " + std::to_string(ws_bytes) +
@@ -409,6 +439,10 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
                 float* dk_loc, float* dv_loc, float* dk_recv, float* dv_recv, void* ws,
                 size_t ws_bytes, void* stream) {
   fc::clear_error();
+  if (int rc = check_aligned({q, k_loc, v_loc, k_recv, v_recv, o, o_f32, dout, dq, dk_loc, dv_loc,
+                               dk_recv, dv_recv, ws},
+                              {lse}))
+    return rc;
   View* v;
   if (int rc = check_view(view, v)) return rc;
   if (v->t_q() == 0) return FC_OK;
@@ -419,9 +453,6 @@ int fc_attn_bwd(fc_view view, const void* q, const void* k_loc, const void* v_lo
   if ((!o && !o_f32) || !q || !k_loc || !v_loc || !lse || !dout || !dq || !dk_loc || !dv_loc ||
       (v->t_recv() && (!k_recv || !v_recv || !dk_recv || !dv_recv)))
     return fail(FC_ERR_INVALID_ARG, "null tensor pointer");
-  if (reinterpret_cast<uintptr_t>(dq) % 16) return fail(FC_ERR_INVALID_ARG, "dq must be 16-byte aligned");
-  if (o_f32 && reinterpret_cast<uintptr_t>(o_f32) % 16)
-    return fail(FC_ERR_INVALID_ARG, "o_f32 must be 16-byte aligned");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   float* delta = static_cast<float*>(ws);
   // the preprocess also zeroes dq for the atomic pass

@@ -221,18 +221,38 @@ def test_kernel_calls_rejected_before_launch():
     plan = P.plan_per_doc(cu, 2)
     v = F.View(cu, plan, 2, 0, 4, 4, 64)
     h = v.handle
-    assert lib.fc_kv_gather(h, 1, 1, 128, 1, 1, 1, 1, None) == -5
-    assert lib.fc_attn_fwd(h, 1, 1, 1, 1, 1, 0.0, 0, 1, None, 1, None, 0, None) == -5
+    a = 256   # a stand-in device address, aligned (nothing is dereferenced)
+    assert lib.fc_kv_gather(h, a, a, 128, a, a, a, a, None) == -5
+    assert lib.fc_attn_fwd(h, a, a, a, a, a, 0.0, 0, a, None, a, None, 0, None) == -5
     for det in (0, 1):
-        assert lib.fc_attn_bwd(h, *([1] * 9), 0.0, det, *([1] * 5), None, 0, None) == -5
-        assert lib.fc_attn_bwd_pass(h, *([1] * 8), 0.0, det, *([1] * 5), None, 0, None) == -5
-        assert lib.fc_attn_bwd_noalloc(h, *([1] * 9), 0.0, det, *([1] * 5), None) == -5
-    assert lib.fc_bwd_preprocess(h, 1, None, 1, 1, None) == -5
-    assert lib.fc_attn_bwd_dkdv(h, *([1] * 8), 0.0, *([1] * 4), None, 0, None) == -5
-    assert lib.fc_attn_fwd_partial(h, 0, 1, 1, 1, 0.0, 1, 1, None) == -5
-    assert lib.fc_attn_fwd_partials(h, 1, 1, 1, 1, 1, 0.0, 1, 1, 1, 1, None) == -5
-    assert lib.fc_lse_merge(1, 1, 1, 1, 4, 2, 96, 1, None, 1, None) == -4
-    assert lib.fc_lse_merge(1, 1, 1, 1, -1, 2, 64, 1, None, 1, None) == -1
+        assert lib.fc_attn_bwd(h, *([a] * 9), 0.0, det, *([a] * 5), None, 0, None) == -5
+        assert lib.fc_attn_bwd_pass(h, *([a] * 8), 0.0, det, *([a] * 5), None, 0, None) == -5
+        assert lib.fc_attn_bwd_noalloc(h, *([a] * 9), 0.0, det, *([a] * 5), None) == -5
+    assert lib.fc_bwd_preprocess(h, a, None, a, a, None) == -5
+    assert lib.fc_attn_bwd_dkdv(h, *([a] * 8), 0.0, *([a] * 4), None, 0, None) == -5
+    assert lib.fc_attn_fwd_partial(h, 0, a, a, a, 0.0, a, a, None) == -5
+    assert lib.fc_attn_fwd_partials(h, a, a, a, a, a, 0.0, a, a, a, a, None) == -5
+    assert lib.fc_lse_merge(a, a, a, a, 4, 2, 96, a, None, a, None) == -4
+    assert lib.fc_lse_merge(a, a, a, a, -1, 2, 64, a, None, a, None) == -1
+    # misaligned pointers are refused first: row tensors and workspaces at 16
+    # bytes, lse / delta at 4 (a + 8 and a + 2)
+    m, s = a + 8, a + 2
+    assert lib.fc_kv_gather(h, a, a, 128, a, m, a, a, None) == -1
+    assert lib.fc_attn_fwd(h, m, a, a, a, a, 0.0, 0, a, None, a, None, 0, None) == -1
+    assert lib.fc_attn_fwd(h, a, a, a, a, a, 0.0, 0, a, None, s, None, 0, None) == -1
+    assert lib.fc_attn_fwd(h, a, a, a, a, a, 0.0, 0, a, None, a, m, 1 << 20, None) == -1
+    assert lib.fc_attn_fwd_partial(h, 0, a, a, a, 0.0, m, a, None) == -1
+    assert lib.fc_attn_fwd_partials(h, a, a, a, a, a, 0.0, a, a, a, s, None) == -1
+    assert lib.fc_lse_merge(a, a, m, a, 4, 2, 64, a, None, a, None) == -1
+    assert lib.fc_lse_merge(a, a, a, a, 4, 2, 64, a, None, s, None) == -1
+    assert lib.fc_bwd_preprocess(h, a, m, a, a, None) == -1
+    assert lib.fc_bwd_preprocess(h, a, None, a, s, None) == -1
+    assert lib.fc_attn_bwd_dkdv(h, *([a] * 6), s, a, 0.0, *([a] * 4), None, 0, None) == -1
+    assert lib.fc_attn_bwd_dq(h, *([a] * 8), 0.0, m, None) == -1
+    for det in (0, 1):
+        assert lib.fc_attn_bwd(h, *([a] * 9), 0.0, det, m, *([a] * 4), None, 0, None) == -1
+        assert lib.fc_attn_bwd(h, *([a] * 9), 0.0, det, *([a] * 5), m, 1 << 20, None) == -1
+        assert lib.fc_attn_bwd_pass(h, *([a] * 6), s, a, 0.0, det, *([a] * 5), None, 0, None) == -1
     f, b, k = v.workspace_size(F.FC_TWO_PASS)
     i = v.info
     # the two-pass forward keeps the received partial's fp32 O (merged in the
